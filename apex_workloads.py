@@ -246,6 +246,12 @@ class DeviceWorkload:
         self.out = torch.empty((B, Hq, d), dtype=torch.float16, device=device)
         self.scale = SCALE
 
+    def to(self, device):
+        """Move every tensor to ``device`` (e.g. a case drawn on the CPU)."""
+        for name in ("q", "k_cache", "v_cache", "block_table", "context_lens", "out"):
+            setattr(self, name, getattr(self, name).to(device))
+        return self
+
     @property
     def algorithmic_bytes(self):
         c = self.cfg

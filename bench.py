@@ -1,0 +1,220 @@
+"""Benchmark: batched paged decode attention, one layer-step, on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload c4]
+
+A step is one apex_decode_attention call (planner + attention + combine
+kernels) over the whole batch with inputs resident in HBM.  W untimed steps,
+then K steps back to back between two device synchronisations.  Prints one
+JSON line:
+
+  value      algorithmic HBM GB/s of the whole step: (KV + Q + O bytes of valid
+             tokens) / (ms per step); us_per_layer_step alongside
+  roofline   the attention kernel alone: algorithmic bytes / its mean duration,
+             timed with HIP events recorded by the library on the launch stream
+             around that kernel, against the 8 TB/s HBM peak; "traffic" is the
+             HBM bytes per launch from the committed rocprofv3 counter summary
+             when it was taken on the current kernel source, else null
+  cpu_baseline  the fp64 CPU oracle on the host cores over a bounded sample of
+             the same workload (the first requests), in the same unit
+
+The default workload is the Llama-3.1-8B GQA long-output decode batch (B=32,
+32 q-heads over 8 kv-heads, d=128, block_size 16, context lengths lognormal
+with median 12k clipped to [4096, 32768]).  Only one GPU is used: --gpus above
+1 is refused.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "decode-attn µs/layer-step + achieved HBM GB/s (% peak), Llama-3.1-8B GQA"
+PEAK_HBM_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2506_03296_amd", "csrc", f)
+                  for f in ("kernels.h", "plan_policy.h", "apex_decode.hip")]
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_digest():
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(workload):
+    """HBM bytes per attention launch from the committed counter summary, if
+    it was taken on the current kernel source and this workload."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    entry = t.get(workload)
+    if not entry or entry.get("source_digest") != kernel_source_digest():
+        return None
+    return entry.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, target_s):
+    """Time the fp64 oracle on the host over the first requests of the batch."""
+    import numpy as np
+
+    import oracle
+    import apex_workloads as W
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    cfg = wl.cfg
+
+    def run(n):
+        case = wl.host_request_case(range(n))
+        t0 = time.perf_counter()
+        oracle.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                    case.context_lens, case.scale, num_threads=threads)
+        return time.perf_counter() - t0, case
+
+    n = 1
+    dt, case = run(n)
+    if dt < target_s:
+        per = dt / n
+        n = int(min(cfg.B, max(1, target_s / max(per, 1e-6))))
+        dt, case = run(n)
+    nbytes = W.algorithmic_bytes(case.context_lens, n, cfg.Hq, cfg.Hkv, cfg.d)
+    return {
+        "value": round(nbytes / dt / 1e9, 4),
+        "unit": "GB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"first {n} of {cfg.B} requests ({int(np.sum(case.context_lens))} tokens, "
+                  f"{nbytes / 1e6:.1f} MB algorithmic), fp64 plain-loop oracle, {dt:.2f} s",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="c4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--items-per-cu", type=int, default=0)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (for counter scaling)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import apex_workloads as W
+    import paper_2506_03296_amd as A
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    A.load_library()
+
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup + args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n, "launches": args.warmup + args.steps}))
+        return
+
+    log(f"generating workload {args.workload}")
+    wl = W.DeviceWorkload(args.workload)
+    cfg = wl.cfg
+    nbytes = wl.algorithmic_bytes
+    torch.cuda.synchronize()
+
+    def step(events=None):
+        A.decode_attention_ex(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens,
+                              wl.scale, out=wl.out, items_per_cu=args.items_per_cu,
+                              events=events)
+
+    log(f"warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev_pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record()
+    for i in range(args.steps):
+        step(ev_pairs[i])
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = start.elapsed_time(stop) / args.steps
+    kern_ms = sorted(a.elapsed_time(b) for a, b in ev_pairs)
+    kern_mean = sum(kern_ms) / len(kern_ms)
+    log(f"{ms_per_step * 1e3:.1f} us/step (wall {wall * 1e6 / args.steps:.1f} us), "
+        f"attention kernel mean {kern_mean * 1e3:.1f} us")
+
+    achieved = nbytes / (kern_mean * 1e-3) / 1e9
+    traffic = committed_traffic(args.workload)
+    result = {
+        "metric": METRIC,
+        "value": round(nbytes / (ms_per_step * 1e-3) / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "us_per_layer_step": round(ms_per_step * 1e3, 2),
+        "pct_of_peak_hbm": round(100.0 * nbytes / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{cfg.name}: {cfg.title}",
+            "B": cfg.B, "Hq": cfg.Hq, "Hkv": cfg.Hkv, "d": cfg.d, "block_size": cfg.block_size,
+            "total_tokens": int(wl.lens.sum()),
+            "algorithmic_bytes": int(nbytes),
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "attn_kernel",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "traffic": traffic,
+            "kernel_us_mean": round(kern_mean * 1e3, 2),
+            "kernel_us_p10": round(kern_ms[len(kern_ms) // 10] * 1e3, 2),
+            "kernel_us_p90": round(kern_ms[(9 * len(kern_ms)) // 10] * 1e3, 2),
+        },
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle")
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

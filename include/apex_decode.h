@@ -1,0 +1,144 @@
+/*
+ * apex_decode.h -- C ABI of the MI355X (gfx950) batched paged decode-attention
+ * library.
+ *
+ * The operation.  In the decode phase each request contributes one query
+ * token per iteration, and the GPU performs self-attention for the requests
+ * assigned to it over their KV pairs resident in GPU memory (APEX, Sec. 3.1
+ * "System Overview" and Sec. 3.3 "Asynchronous Overlap Mechanism"); the KV
+ * cache is paged (Sec. 4.1) and the bandwidth-bound nature of this decode
+ * attention is what APEX's placement decisions revolve around (Sec. 2.2).
+ * APEX changes only where attention runs, never its mathematics (Sec. 3.1).
+ * For request b with L_b = context_lens[b] cached tokens and q-head h:
+ *
+ *     out[b][h] = sum_t softmax_t(scale * q[b][h] . K_t) * V_t,  t in [0, L_b)
+ *
+ * where token t lives in physical block block_table[b][t / block_size] at slot
+ * t % block_size, and q-head h reads kv-head h / (Hq / Hkv).
+ *
+ * Layouts (all device memory, row-major, contiguous, 16-byte aligned):
+ *   q            fp16  [B][Hq][d]          (rotary embedding already applied)
+ *   k_cache      fp16  [num_blocks][Hkv][block_size][d]
+ *   v_cache      fp16  same layout as k_cache
+ *   block_table  int32 [B][stride]; in apex_decode_attention the stride is
+ *                tight, ceil(max_b L_b / block_size), and is derived on the
+ *                device; entries past ceil(L_b / block_size) are never read
+ *   context_lens int32 [B]; counts the current token (its K/V must already be
+ *                in the cache); L_b <= 0 yields a zero output row
+ *   out          fp16  [B][Hq][d]; must not overlap q
+ *
+ * Supported: d = 128, block_size = 16, Hq % Hkv == 0 with Hq / Hkv in
+ * {1, 2, 4, 8}.  Anything else returns APEX_ERR_UNSUPPORTED.
+ *
+ * Precision: fp16 inputs, fp32 scores, softmax statistics and accumulation,
+ * fp16 output rounded to nearest even.
+ *
+ * Ownership: the caller owns every buffer; the library never retains or
+ * frees caller pointers.  Calls are asynchronous: they validate arguments on
+ * the host, enqueue kernels on `stream` (a hipStream_t; NULL = the legacy
+ * default stream) and return without synchronising.  Nothing is printed and
+ * no C++ exception crosses this boundary.
+ *
+ * Errors: every entry point returns an apex_status; on failure nothing has
+ * been enqueued and apex_decode_last_error() returns a message
+ * (thread-local).  Block ids out of range are not checked on the device.
+ */
+#ifndef APEX_DECODE_H
+#define APEX_DECODE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum apex_status {
+    APEX_OK = 0,
+    APEX_ERR_INVALID_ARG = -1,   /* null/misaligned pointer, B < 0, Hq % Hkv != 0, aliasing */
+    APEX_ERR_UNSUPPORTED = -2,   /* d, block_size or group size outside the supported set */
+    APEX_ERR_OUT_OF_MEMORY = -3, /* workspace allocation failed or caller workspace too small */
+    APEX_ERR_HIP = -4            /* a HIP runtime call or kernel launch failed */
+} apex_status;
+
+/*
+ * Batched paged decode attention for one layer-step (the formula above).
+ * B == 0 is a successful no-op.  Uses a library-owned, lazily grown workspace
+ * per device; concurrent calls on different streams of one device must use
+ * apex_decode_attention_ex with caller-owned workspaces.
+ */
+int apex_decode_attention(const void* q, const void* k_cache, const void* v_cache,
+                          const int32_t* block_table, const int32_t* context_lens, void* out,
+                          int B, int Hq, int Hkv, int d, int block_size, float scale,
+                          void* stream);
+
+/* Extended arguments.  Zero-initialise and fill the first group; every
+ * extension field has "off" as its zero value. */
+typedef struct apex_decode_args {
+    /* same meaning as the apex_decode_attention arguments */
+    const void* q;
+    const void* k_cache;
+    const void* v_cache;
+    const int32_t* block_table;
+    const int32_t* context_lens;
+    void* out;
+    int B, Hq, Hkv, d, block_size;
+    float scale;
+    void* stream;
+
+    /* entries per block_table row; 0 = tight (derived on the device) */
+    int64_t block_table_stride;
+    /* 0 = the split-K planner sizes the splits; n > 0 splits every request
+     * with L_b > 0 into exactly n block-aligned token ranges of
+     * ceil(blocks / n) blocks each (trailing ranges may be empty) */
+    int num_splits;
+    /* target work items per compute unit for the planner; 0 = default */
+    int items_per_cu;
+    /* caller-owned device workspace of at least apex_decode_workspace_bytes()
+     * bytes, or NULL for the library-owned one */
+    void* workspace;
+    size_t workspace_bytes;
+    /* optional fp32 [B][Hq]: natural-log log-sum-exp of the scaled logits
+     * (max + log of the normaliser); -inf for L_b <= 0 */
+    float* lse_out;
+    /* optional pair of hipEvent_t recorded on `stream` immediately before and
+     * after the attention kernel (for per-kernel timing); NULL = none */
+    void* attn_kernel_events[2];
+    uint32_t flags; /* reserved, must be 0 */
+} apex_decode_args;
+
+int apex_decode_attention_ex(const apex_decode_args* args);
+
+/* Workspace bytes a call with these shapes needs on the current device
+ * (num_splits and items_per_cu as in apex_decode_args).  0 on bad shapes. */
+size_t apex_decode_workspace_bytes(int B, int Hq, int Hkv, int d, int block_size,
+                                   int num_splits, int items_per_cu);
+
+/*
+ * Host mirror of the split-K partition policy, for inspection and tests (no
+ * GPU needed).  Inputs: host context_lens[B], Hkv, block_size, the compute
+ * unit count to plan for, num_splits / items_per_cu as in apex_decode_args.
+ * Outputs (host arrays of B entries, any may be NULL): splits_out[b] = number
+ * of token ranges of request b, blocks_per_split_out[b] = blocks per range.
+ * *chunk_out = planner chunk in blocks, *items_out = work items (ranges x
+ * Hkv), *partial_slots_out = ranges that write partial results.
+ */
+int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block_size,
+                          int num_cu, int num_splits, int items_per_cu, int32_t* splits_out,
+                          int32_t* blocks_per_split_out, int64_t* chunk_out, int64_t* items_out,
+                          int64_t* partial_slots_out);
+
+/* Message for the last failed call on this thread ("" if none). */
+const char* apex_decode_last_error(void);
+
+/* Frees the library-owned workspaces (waits for the devices first). */
+int apex_decode_release_workspace(void);
+
+/* Library version: major * 10000 + minor * 100 + patch. */
+int apex_decode_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* APEX_DECODE_H */

@@ -1,0 +1,219 @@
+"""Python binding of libapex_decode.so: batched paged decode attention on MI355X.
+
+Argument marshalling only.  Every step of the attention runs in the HIP
+kernels of the library; torch provides device memory and the current stream.
+If the built library is missing, importing the binding's functions raises --
+there is no fallback.
+
+    out = decode_attention(q, k_cache, v_cache, block_table, context_lens, scale)
+
+q [B][Hq][128] fp16, caches [num_blocks][Hkv][16][128] fp16, block_table int32
+[B][stride], context_lens int32 [B] (all on the same GPU).  The names and
+argument order follow include/apex_decode.h.
+"""
+import ctypes
+import os
+
+__all__ = [
+    "ApexError", "LIB_PATH", "load_library", "decode_attention", "decode_attention_ex",
+    "workspace_bytes", "plan_host", "last_error", "release_workspace", "version",
+    "APEX_OK", "APEX_ERR_INVALID_ARG", "APEX_ERR_UNSUPPORTED", "APEX_ERR_OUT_OF_MEMORY",
+    "APEX_ERR_HIP", "EXPORTED_SYMBOLS",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libapex_decode.so")
+
+APEX_OK = 0
+APEX_ERR_INVALID_ARG = -1
+APEX_ERR_UNSUPPORTED = -2
+APEX_ERR_OUT_OF_MEMORY = -3
+APEX_ERR_HIP = -4
+
+EXPORTED_SYMBOLS = (
+    "apex_decode_attention", "apex_decode_attention_ex", "apex_decode_workspace_bytes",
+    "apex_decode_plan_host", "apex_decode_last_error", "apex_decode_release_workspace",
+    "apex_decode_version",
+)
+
+
+class ApexError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"apex_decode error {code}: {msg}")
+        self.code = code
+
+
+class DecodeArgs(ctypes.Structure):
+    """Mirror of apex_decode_args (include/apex_decode.h)."""
+    _fields_ = [
+        ("q", ctypes.c_void_p), ("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p),
+        ("block_table", ctypes.c_void_p), ("context_lens", ctypes.c_void_p),
+        ("out", ctypes.c_void_p),
+        ("B", ctypes.c_int), ("Hq", ctypes.c_int), ("Hkv", ctypes.c_int), ("d", ctypes.c_int),
+        ("block_size", ctypes.c_int), ("scale", ctypes.c_float), ("stream", ctypes.c_void_p),
+        ("block_table_stride", ctypes.c_int64), ("num_splits", ctypes.c_int),
+        ("items_per_cu", ctypes.c_int), ("workspace", ctypes.c_void_p),
+        ("workspace_bytes", ctypes.c_size_t), ("lse_out", ctypes.c_void_p),
+        ("attn_kernel_events", ctypes.c_void_p * 2), ("flags", ctypes.c_uint32),
+    ]
+
+
+_LIB = None
+
+
+def load_library(path=None):
+    """Load (once) and return the ctypes handle of libapex_decode.so."""
+    global _LIB
+    if _LIB is not None and path is None:
+        return _LIB
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise ApexError(APEX_ERR_HIP, f"{p} is not built; run __graft_entry__.build() "
+                                      "(python -m paper_2506_03296_amd.build)")
+    lib = ctypes.CDLL(p)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
+    lib.apex_decode_attention.restype = i32
+    lib.apex_decode_attention.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32,
+                                          ctypes.c_float, vp]
+    lib.apex_decode_attention_ex.restype = i32
+    lib.apex_decode_attention_ex.argtypes = [ctypes.POINTER(DecodeArgs)]
+    lib.apex_decode_workspace_bytes.restype = ctypes.c_size_t
+    lib.apex_decode_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32, i32]
+    lib.apex_decode_plan_host.restype = i32
+    lib.apex_decode_plan_host.argtypes = [vp, i32, i32, i32, i32, i32, i32, vp, vp,
+                                          ctypes.POINTER(i64), ctypes.POINTER(i64),
+                                          ctypes.POINTER(i64)]
+    lib.apex_decode_last_error.restype = ctypes.c_char_p
+    lib.apex_decode_last_error.argtypes = []
+    lib.apex_decode_release_workspace.restype = i32
+    lib.apex_decode_release_workspace.argtypes = []
+    lib.apex_decode_version.restype = i32
+    lib.apex_decode_version.argtypes = []
+    if path is None:
+        _LIB = lib
+    return lib
+
+
+def last_error():
+    return load_library().apex_decode_last_error().decode()
+
+
+def _check(rc):
+    if rc != APEX_OK:
+        raise ApexError(rc, last_error())
+
+
+def version():
+    return load_library().apex_decode_version()
+
+
+def release_workspace():
+    _check(load_library().apex_decode_release_workspace())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _addr(t):
+    return None if t is None else int(t.data_ptr())
+
+
+def _event_handle(ev, stream):
+    """Raw hipEvent_t of a torch.cuda.Event (created on first use)."""
+    if not ev.cuda_event:
+        ev.record(stream)
+    return int(ev.cuda_event)
+
+
+def _stream_obj(stream, device):
+    import torch
+    return stream if stream is not None else torch.cuda.current_stream(device)
+
+
+def _stream_handle(stream, device):
+    return ctypes.c_void_p(_stream_obj(stream, device).cuda_stream)
+
+
+def _shapes(q, k_cache):
+    if q.dim() != 3 or k_cache.dim() != 4:
+        raise ValueError("q must be [B][Hq][d] and the caches [num_blocks][Hkv][block_size][d]")
+    B, Hq, d = q.shape
+    _, Hkv, bs, dk = k_cache.shape
+    if dk != d:
+        raise ValueError("q and the caches disagree on the head dim")
+    return B, Hq, Hkv, d, bs
+
+
+def decode_attention(q, k_cache, v_cache, block_table, context_lens, scale, out=None,
+                     stream=None):
+    """apex_decode_attention over torch tensors; returns ``out``.
+
+    The block table must be tight ([B][ceil(max L / 16)]); use
+    ``decode_attention_ex`` for wider rows."""
+    import torch
+    B, Hq, Hkv, d, bs = _shapes(q, k_cache)
+    if out is None:
+        out = torch.empty((B, Hq, d), dtype=torch.float16, device=q.device)
+    lib = load_library()
+    rc = lib.apex_decode_attention(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                                   _ptr(context_lens), _ptr(out), B, Hq, Hkv, d, bs,
+                                   ctypes.c_float(scale), _stream_handle(stream, q.device))
+    _check(rc)
+    return out
+
+
+def decode_attention_ex(q, k_cache, v_cache, block_table, context_lens, scale, out=None,
+                        block_table_stride=0, num_splits=0, items_per_cu=0, workspace=None,
+                        lse_out=None, events=None, stream=None):
+    """apex_decode_attention_ex over torch tensors; returns ``out``.
+
+    ``workspace`` is an optional uint8 device tensor (caller-owned);
+    ``events`` an optional pair of torch.cuda.Event recorded around the
+    attention kernel."""
+    import torch
+    B, Hq, Hkv, d, bs = _shapes(q, k_cache)
+    if out is None:
+        out = torch.empty((B, Hq, d), dtype=torch.float16, device=q.device)
+    a = DecodeArgs()
+    a.q, a.k_cache, a.v_cache = _addr(q), _addr(k_cache), _addr(v_cache)
+    a.block_table, a.context_lens, a.out = _addr(block_table), _addr(context_lens), _addr(out)
+    a.B, a.Hq, a.Hkv, a.d, a.block_size = B, Hq, Hkv, d, bs
+    a.scale = float(scale)
+    s = _stream_obj(stream, q.device)
+    a.stream = int(s.cuda_stream)
+    a.block_table_stride = int(block_table_stride)
+    a.num_splits = int(num_splits)
+    a.items_per_cu = int(items_per_cu)
+    if workspace is not None:
+        a.workspace = _addr(workspace)
+        a.workspace_bytes = workspace.numel() * workspace.element_size()
+    a.lse_out = _addr(lse_out)
+    if events is not None:
+        a.attn_kernel_events[0] = _event_handle(events[0], s)
+        a.attn_kernel_events[1] = _event_handle(events[1], s)
+    _check(load_library().apex_decode_attention_ex(ctypes.byref(a)))
+    return out
+
+
+def workspace_bytes(B, Hq, Hkv, d=128, block_size=16, num_splits=0, items_per_cu=0):
+    return int(load_library().apex_decode_workspace_bytes(B, Hq, Hkv, d, block_size,
+                                                          num_splits, items_per_cu))
+
+
+def plan_host(context_lens, Hkv, num_cu, block_size=16, num_splits=0, items_per_cu=0):
+    """Host mirror of the split-K policy (no GPU).  Returns a dict with
+    per-request 'splits' and 'blocks_per_split' (numpy int32) and the scalars
+    'chunk', 'items' and 'partial_slots'."""
+    import numpy as np
+    lens = np.ascontiguousarray(np.asarray(context_lens), dtype=np.int32)
+    B = lens.shape[0]
+    splits = np.zeros(max(B, 1), dtype=np.int32)
+    per = np.zeros(max(B, 1), dtype=np.int32)
+    chunk, items, slots = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    rc = load_library().apex_decode_plan_host(
+        lens.ctypes.data if B else None, B, Hkv, block_size, num_cu, num_splits, items_per_cu,
+        splits.ctypes.data, per.ctypes.data, ctypes.byref(chunk), ctypes.byref(items),
+        ctypes.byref(slots))
+    _check(rc)
+    return {"splits": splits[:B], "blocks_per_split": per[:B], "chunk": chunk.value,
+            "items": items.value, "partial_slots": slots.value}

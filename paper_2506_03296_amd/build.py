@@ -1,0 +1,35 @@
+"""Build the gfx950 HIP library libapex_decode.so in-tree with hipcc."""
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(HERE, "csrc")
+LIB = os.path.join(HERE, "libapex_decode.so")
+SOURCES = [os.path.join(CSRC, "apex_decode.hip")]
+HEADERS = [os.path.join(ROOT, "include", "apex_decode.h"),
+           os.path.join(CSRC, "kernels.h"), os.path.join(CSRC, "plan_policy.h")]
+
+HIPCC_FLAGS = [
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "-Wall", "-Wno-unused-function",
+    # packed fp32 VALU forms stay off (compiler emits plain fp32 ops instead)
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+]
+
+
+def build(out=LIB, extra=(), quiet=False):
+    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    cmd = [hipcc, *HIPCC_FLAGS, *extra, *SOURCES, "-o", out + ".tmp"]
+    if not quiet:
+        print(" ".join(cmd), flush=True)
+    subprocess.check_call(cmd)
+    os.replace(out + ".tmp", out)
+    return out
+
+
+if __name__ == "__main__":
+    build()
+    sys.exit(0)

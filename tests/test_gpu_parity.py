@@ -1,0 +1,246 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Bar (fp16 outputs, fp32 accumulation): every output finite, max-abs error
+<= 2e-3 and relative L2 error <= 1e-3 against the unrounded fp64 oracle.
+Small cases are compared element by element; the full-size workloads run in
+the launch configuration the benchmark times and are compared on sampled
+requests (the oracle computes those requests one by one).
+"""
+import numpy as np
+import pytest
+
+import apex_workloads as W
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS = 2e-3
+REL_L2 = 1e-3
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+@pytest.fixture(scope="module")
+def apex():
+    import paper_2506_03296_amd as A
+    A.load_library()
+    return A
+
+
+def to_dev(torch, case):
+    dev = "cuda"
+    return (torch.from_numpy(case.q).to(dev), torch.from_numpy(case.k_cache).to(dev),
+            torch.from_numpy(case.v_cache).to(dev), torch.from_numpy(case.block_table).to(dev),
+            torch.from_numpy(case.context_lens).to(dev))
+
+
+def run_gpu(torch, apex, case, **kw):
+    q, k, v, bt, lens = to_dev(torch, case)
+    if kw:
+        out = apex.decode_attention_ex(q, k, v, bt, lens, case.scale, **kw)
+    else:
+        out = apex.decode_attention(q, k, v, bt, lens, case.scale)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def assert_parity(got, ref, what=""):
+    got = np.asarray(got, dtype=np.float64)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite outputs"
+    err = np.abs(got - ref)
+    max_abs = float(err.max()) if err.size else 0.0
+    nrm = float(np.linalg.norm(ref))
+    rel = float(np.linalg.norm(got - ref)) / nrm if nrm > 0 else float(np.linalg.norm(got))
+    print(f"[parity] {what}: max_abs={max_abs:.3e} rel_l2={rel:.3e}", flush=True)
+    assert max_abs <= MAX_ABS, f"{what}: max-abs {max_abs:.3e}"
+    assert rel <= REL_L2, f"{what}: rel-L2 {rel:.3e}"
+
+
+# ---------------------------------------------------------------------------
+# small cases, element by element
+# ---------------------------------------------------------------------------
+
+def test_c1_tiny_mha_full_parity(torch_cuda, apex, oracle_mod):
+    torch = torch_cuda
+    wl = W.DeviceWorkload("c1", device="cpu").to("cuda")
+    out = apex.decode_attention(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens,
+                                wl.scale)
+    torch.cuda.synchronize()
+    ref = oracle_mod.decode_attention_f64(wl.q.cpu().numpy(), wl.k_cache.cpu().numpy(),
+                                          wl.v_cache.cpu().numpy(), wl.block_table.cpu().numpy(),
+                                          wl.context_lens.cpu().numpy(), wl.scale)
+    assert_parity(out.cpu().numpy(), ref, "c1")
+
+
+SMALL = [
+    # name, lens, Hq, Hkv
+    ("mha_ragged", [1, 15, 16, 17, 100, 511], 8, 8),
+    ("g2_ragged", [33, 0, 250, 64, 7], 8, 4),
+    ("g4_ragged", [1, 2, 31, 32, 33, 1000, 3001], 16, 4),
+    ("g8_ragged", [5, 129, 700], 16, 2),
+    ("g4_long", [9000, 40, 2500], 32, 8),
+    ("mha_many", list(range(1, 400, 37)), 4, 4),
+]
+
+
+@pytest.mark.parametrize("name,lens,Hq,Hkv", SMALL, ids=[s[0] for s in SMALL])
+@pytest.mark.parametrize("splits", [0, 1, 2, 7, 64])
+def test_small_cases_with_poison(torch_cuda, apex, oracle_mod, name, lens, Hq, Hkv, splits):
+    case = W.make_host_case(lens, Hq, Hkv, seed=len(lens) * 31 + Hq, poison=True)
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale)
+    got = run_gpu(torch_cuda, apex, case, num_splits=splits)
+    assert_parity(got, ref, f"{name} splits={splits}")
+    for b, L in enumerate(lens):
+        if L == 0:
+            assert np.all(got[b] == 0)
+
+
+def test_lse_output(torch_cuda, apex, oracle_mod):
+    torch = torch_cuda
+    case = W.make_host_case([1, 70, 0, 3000], 16, 4, seed=77)
+    _, lse_ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache,
+                                                 case.block_table, case.context_lens, case.scale,
+                                                 return_lse=True)
+    for splits in (0, 1, 5):
+        lse = torch.empty((4, 16), dtype=torch.float32, device="cuda")
+        run_gpu(torch, apex, case, num_splits=splits, lse_out=lse)
+        got = lse.cpu().numpy().astype(np.float64)
+        assert np.all(np.isneginf(got[2]))
+        fin = np.isfinite(lse_ref)
+        assert np.max(np.abs(got[fin] - lse_ref[fin])) < 1e-4
+
+
+def test_wide_block_table_stride(torch_cuda, apex, oracle_mod):
+    case = W.make_host_case([40, 300, 17], 8, 2, seed=5, stride=64)
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale)
+    got = run_gpu(torch_cuda, apex, case, block_table_stride=64)
+    assert_parity(got, ref, "stride=64")
+
+
+def test_caller_workspace_and_side_stream(torch_cuda, apex, oracle_mod):
+    torch = torch_cuda
+    case = W.make_host_case([500, 5, 2000], 32, 8, seed=6)
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale)
+    q, k, v, bt, lens = to_dev(torch, case)
+    nbytes = apex.workspace_bytes(3, 32, 8)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        out = apex.decode_attention_ex(q, k, v, bt, lens, case.scale, workspace=ws, stream=s)
+    s.synchronize()
+    assert_parity(out.cpu().numpy(), ref, "caller workspace, side stream")
+    small = torch.empty(256, dtype=torch.uint8, device="cuda")
+    with pytest.raises(apex.ApexError) as e:
+        apex.decode_attention_ex(q, k, v, bt, lens, case.scale, workspace=small)
+    assert e.value.code == apex.APEX_ERR_OUT_OF_MEMORY
+
+
+# ---------------------------------------------------------------------------
+# invariants on the GPU path
+# ---------------------------------------------------------------------------
+
+def test_single_token_returns_v_bitwise(torch_cuda, apex):
+    case = W.make_host_case([1, 1, 1, 1], 32, 8, seed=8, poison=True)
+    got = run_gpu(torch_cuda, apex, case)
+    for b in range(4):
+        blk = case.block_table[b, 0]
+        exp = np.repeat(case.v_cache[blk, :, 0], 4, axis=0)
+        assert np.array_equal(got[b].astype(np.float16), exp)
+
+
+def test_identical_keys_give_mean_of_v(torch_cuda, apex):
+    case = W.make_host_case([3, 77, 1200], 32, 8, seed=9)
+    key = np.random.default_rng(1).standard_normal((8, 128)).astype(np.float16)
+    case.k_cache[:] = key[None, :, None, :]
+    got = run_gpu(torch_cuda, apex, case)
+    from oracle import brute_force
+    for b, L in enumerate(case.context_lens):
+        V = brute_force.dense_kv(case.v_cache, case.block_table, b, int(L))
+        mean = np.repeat(V.mean(axis=1), 4, axis=0)
+        assert np.max(np.abs(got[b] - mean)) <= MAX_ABS
+
+
+def test_unit_values_give_unit_output(torch_cuda, apex):
+    case = W.make_host_case([1, 50, 5000], 32, 8, seed=10)
+    case.v_cache[:] = 1
+    for splits in (0, 3):
+        got = run_gpu(torch_cuda, apex, case, num_splits=splits)
+        assert np.all(got == 1.0)
+
+
+def test_block_permutation_is_bitwise_invariant(torch_cuda, apex):
+    case = W.make_host_case([100, 1, 2048, 333], 32, 8, seed=11, slack_blocks=5)
+    base = run_gpu(torch_cuda, apex, case)
+    perm = np.random.default_rng(2).permutation(case.k_cache.shape[0])
+    k2 = np.empty_like(case.k_cache)
+    v2 = np.empty_like(case.v_cache)
+    k2[perm] = case.k_cache
+    v2[perm] = case.v_cache
+    case.k_cache, case.v_cache = k2, v2
+    case.block_table = perm[case.block_table].astype(np.int32)
+    assert np.array_equal(run_gpu(torch_cuda, apex, case), base)
+
+
+def test_gqa_matches_mha_with_repeated_kv(torch_cuda, apex):
+    case = W.make_host_case([64, 900, 3], 32, 8, seed=12)
+    gqa = run_gpu(torch_cuda, apex, case)
+    case.k_cache = np.ascontiguousarray(np.repeat(case.k_cache, 4, axis=1))
+    case.v_cache = np.ascontiguousarray(np.repeat(case.v_cache, 4, axis=1))
+    mha = run_gpu(torch_cuda, apex, case)
+    assert np.max(np.abs(gqa.astype(np.float64) - mha)) <= 1e-3
+
+
+def test_late_peaked_key_dominates(torch_cuda, apex, oracle_mod):
+    case = W.make_host_case([4000], 4, 1, seed=13)
+    q = case.q[0, 0].astype(np.float64)
+    t = 3990
+    blk = case.block_table[0, t // 16]
+    case.k_cache[blk, 0, t % 16] = (40.0 * q / np.linalg.norm(q)).astype(np.float16)
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale)
+    for splits in (0, 1, 9):
+        assert_parity(run_gpu(torch_cuda, apex, case, num_splits=splits), ref, f"peaked splits={splits}")
+
+
+def test_repeated_runs_are_bitwise_identical(torch_cuda, apex):
+    case = W.make_host_case([3000, 17, 900, 4500], 32, 8, seed=14)
+    a = run_gpu(torch_cuda, apex, case)
+    b = run_gpu(torch_cuda, apex, case)
+    assert np.array_equal(a, b)
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads, sampled requests, in the benchmark's launch configuration
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["c2", "c3", "c4", "c5"])
+def test_full_size_sampled_parity(torch_cuda, apex, oracle_mod, name):
+    torch = torch_cuda
+    print(f"[full-size] generating {name}", flush=True)
+    wl = W.DeviceWorkload(name)
+    apex.decode_attention(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens,
+                          wl.scale, out=wl.out)
+    torch.cuda.synchronize()
+    out = wl.out.float()
+    assert bool(torch.isfinite(out).all())
+    lens = wl.lens
+    rng = np.random.default_rng(100)
+    picks = {int(np.argmax(lens)), int(np.argmin(lens)), 0, len(lens) - 1}
+    picks.update(int(x) for x in rng.choice(len(lens), size=4, replace=False))
+    picks = sorted(picks)
+    case = wl.host_request_case(picks)
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale)
+    got = out[torch.tensor(picks, device="cuda")].cpu().numpy()
+    assert_parity(got, ref, f"{name} requests {picks}")
+    del wl
+    torch.cuda.empty_cache()
