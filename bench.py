@@ -2,8 +2,8 @@
 
     python bench.py [--steps K] [--warmup W] [--workload c4]
 
-A step is one apex_decode_attention call (planner + attention + combine
-kernels) over the whole batch with inputs resident in HBM.  W untimed steps,
+A step is one apex_decode_attention call (one persistent kernel that plans,
+attends and combines) over the whole batch with inputs resident in HBM.  W untimed steps,
 then K steps back to back between two device synchronisations.  Prints one
 JSON line:
 
@@ -107,9 +107,12 @@ def main():
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--items-per-cu", type=int, default=0)
+    ap.add_argument("--workers", type=int, default=0,
+                    help="work groups of the persistent launch (0 = device default)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (for counter scaling)")
+    ap.add_argument("--hbm-probe", action="store_true",
+                    help="only measure achievable HBM read bandwidth (stream and 4 KiB gather)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -137,6 +140,16 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": n, "launches": args.warmup + args.steps}))
         return
 
+    if args.hbm_probe:
+        from paper_2506_03296_amd import hbm_probe
+        props = torch.cuda.get_device_properties(0)
+        cus = props.multi_processor_count
+        res = hbm_probe.measure(blocks_list=(cus * 2, cus * 4, cus * 8, cus * 16, cus * 32))
+        res["device"] = props.name
+        res["cus"] = cus
+        print(json.dumps(res), flush=True)
+        return
+
     log(f"generating workload {args.workload}")
     wl = W.DeviceWorkload(args.workload)
     cfg = wl.cfg
@@ -145,7 +158,7 @@ def main():
 
     def step(events=None):
         A.decode_attention_ex(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens,
-                              wl.scale, out=wl.out, items_per_cu=args.items_per_cu,
+                              wl.scale, out=wl.out, num_workers=args.workers,
                               events=events)
 
     log(f"warmup {args.warmup}")

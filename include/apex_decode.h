@@ -42,6 +42,12 @@
  * Errors: every entry point returns an apex_status; on failure nothing has
  * been enqueued and apex_decode_last_error() returns a message
  * (thread-local).  Block ids out of range are not checked on the device.
+ *
+ * Work partition: one persistent kernel launch per call.  Each work group
+ * derives the partition from context_lens itself, takes an equal share of
+ * the (request, kv-head, block) units, and (request, kv-head) pairs shared by
+ * several work groups are merged by a log-sum-exp combine done by the last
+ * work group to finish its share of the pair.
  */
 #ifndef APEX_DECODE_H
 #define APEX_DECODE_H
@@ -63,9 +69,10 @@ typedef enum apex_status {
 
 /*
  * Batched paged decode attention for one layer-step (the formula above).
- * B == 0 is a successful no-op.  Uses a library-owned, lazily grown workspace
- * per device; concurrent calls on different streams of one device must use
- * apex_decode_attention_ex with caller-owned workspaces.
+ * B == 0 is a successful no-op.  Uses library-owned workspaces, one set per
+ * device, grown on demand (growing waits for the device); concurrent calls on
+ * different streams of one device must use apex_decode_attention_ex with
+ * caller-owned workspaces.
  */
 int apex_decode_attention(const void* q, const void* k_cache, const void* v_cache,
                           const int32_t* block_table, const int32_t* context_lens, void* out,
@@ -88,14 +95,16 @@ typedef struct apex_decode_args {
 
     /* entries per block_table row; 0 = tight (derived on the device) */
     int64_t block_table_stride;
-    /* 0 = the split-K planner sizes the splits; n > 0 splits every request
-     * with L_b > 0 into exactly n block-aligned token ranges of
-     * ceil(blocks / n) blocks each (trailing ranges may be empty) */
-    int num_splits;
-    /* target work items per compute unit for the planner; 0 = default */
-    int items_per_cu;
+    /* work groups of the persistent launch; 0 = as many as the device keeps
+     * resident.  The work (one unit = one 16-token block of one kv-head) is
+     * cut into equal contiguous ranges, one per work group; with 0 a range is
+     * never shorter than 8 units, with n > 0 every range holds at least one
+     * unit (tests use this to force split requests) */
+    int num_workers;
     /* caller-owned device workspace of at least apex_decode_workspace_bytes()
-     * bytes, or NULL for the library-owned one */
+     * bytes and 256-byte aligned, or NULL for the library-owned one.  Its
+     * first apex_decode_counter_bytes(B, Hkv) bytes must be zero when the call
+     * is enqueued; every call leaves them zero again when it completes. */
     void* workspace;
     size_t workspace_bytes;
     /* optional fp32 [B][Hq]: natural-log log-sum-exp of the scaled logits
@@ -110,23 +119,25 @@ typedef struct apex_decode_args {
 int apex_decode_attention_ex(const apex_decode_args* args);
 
 /* Workspace bytes a call with these shapes needs on the current device
- * (num_splits and items_per_cu as in apex_decode_args).  0 on bad shapes. */
-size_t apex_decode_workspace_bytes(int B, int Hq, int Hkv, int d, int block_size,
-                                   int num_splits, int items_per_cu);
+ * (num_workers as in apex_decode_args).  0 on bad shapes. */
+size_t apex_decode_workspace_bytes(int B, int Hq, int Hkv, int d, int block_size, int num_workers);
+
+/* Leading workspace bytes (arrival counters) that must be zero before a call. */
+size_t apex_decode_counter_bytes(int B, int Hkv);
 
 /*
- * Host mirror of the split-K partition policy, for inspection and tests (no
- * GPU needed).  Inputs: host context_lens[B], Hkv, block_size, the compute
- * unit count to plan for, num_splits / items_per_cu as in apex_decode_args.
- * Outputs (host arrays of B entries, any may be NULL): splits_out[b] = number
- * of token ranges of request b, blocks_per_split_out[b] = blocks per range.
- * *chunk_out = planner chunk in blocks, *items_out = work items (ranges x
- * Hkv), *partial_slots_out = ranges that write partial results.
+ * Host mirror of the work partition, for inspection and tests (no GPU
+ * needed).  Inputs: host context_lens[B], Hkv, block_size, the number of
+ * launched work groups, and whether that number was forced (num_workers > 0
+ * in apex_decode_args).  Outputs (any may be NULL): contributors_out[B * Hkv]
+ * = work groups that share each (request, kv-head) pair (1 = written
+ * directly, more = combined from partials), *units_out = blocks x kv-heads,
+ * *active_out = work groups that get units, *partials_out = partial results
+ * written.
  */
 int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block_size,
-                          int num_cu, int num_splits, int items_per_cu, int32_t* splits_out,
-                          int32_t* blocks_per_split_out, int64_t* chunk_out, int64_t* items_out,
-                          int64_t* partial_slots_out);
+                          int launched_workers, int forced, int32_t* contributors_out,
+                          int64_t* units_out, int64_t* active_out, int64_t* partials_out);
 
 /* Message for the last failed call on this thread ("" if none). */
 const char* apex_decode_last_error(void);

@@ -18,7 +18,7 @@ __all__ = [
     "ApexError", "LIB_PATH", "load_library", "decode_attention", "decode_attention_ex",
     "workspace_bytes", "plan_host", "last_error", "release_workspace", "version",
     "APEX_OK", "APEX_ERR_INVALID_ARG", "APEX_ERR_UNSUPPORTED", "APEX_ERR_OUT_OF_MEMORY",
-    "APEX_ERR_HIP", "EXPORTED_SYMBOLS",
+    "APEX_ERR_HIP", "EXPORTED_SYMBOLS", "counter_bytes",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libapex_decode.so")
@@ -31,8 +31,8 @@ APEX_ERR_HIP = -4
 
 EXPORTED_SYMBOLS = (
     "apex_decode_attention", "apex_decode_attention_ex", "apex_decode_workspace_bytes",
-    "apex_decode_plan_host", "apex_decode_last_error", "apex_decode_release_workspace",
-    "apex_decode_version",
+    "apex_decode_counter_bytes", "apex_decode_plan_host", "apex_decode_last_error",
+    "apex_decode_release_workspace", "apex_decode_version",
 )
 
 
@@ -50,8 +50,8 @@ class DecodeArgs(ctypes.Structure):
         ("out", ctypes.c_void_p),
         ("B", ctypes.c_int), ("Hq", ctypes.c_int), ("Hkv", ctypes.c_int), ("d", ctypes.c_int),
         ("block_size", ctypes.c_int), ("scale", ctypes.c_float), ("stream", ctypes.c_void_p),
-        ("block_table_stride", ctypes.c_int64), ("num_splits", ctypes.c_int),
-        ("items_per_cu", ctypes.c_int), ("workspace", ctypes.c_void_p),
+        ("block_table_stride", ctypes.c_int64), ("num_workers", ctypes.c_int),
+        ("workspace", ctypes.c_void_p),
         ("workspace_bytes", ctypes.c_size_t), ("lse_out", ctypes.c_void_p),
         ("attn_kernel_events", ctypes.c_void_p * 2), ("flags", ctypes.c_uint32),
     ]
@@ -66,6 +66,12 @@ def load_library(path=None):
     if _LIB is not None and path is None:
         return _LIB
     p = path or LIB_PATH
+    try:
+        # torch ships its own HIP runtime; loading it first lets this library
+        # bind to that same runtime instead of a second copy from /opt/rocm
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     if not os.path.exists(p):
         raise ApexError(APEX_ERR_HIP, f"{p} is not built; run __graft_entry__.build() "
                                       "(python -m paper_2506_03296_amd.build)")
@@ -77,9 +83,11 @@ def load_library(path=None):
     lib.apex_decode_attention_ex.restype = i32
     lib.apex_decode_attention_ex.argtypes = [ctypes.POINTER(DecodeArgs)]
     lib.apex_decode_workspace_bytes.restype = ctypes.c_size_t
-    lib.apex_decode_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32, i32]
+    lib.apex_decode_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
+    lib.apex_decode_counter_bytes.restype = ctypes.c_size_t
+    lib.apex_decode_counter_bytes.argtypes = [i32, i32]
     lib.apex_decode_plan_host.restype = i32
-    lib.apex_decode_plan_host.argtypes = [vp, i32, i32, i32, i32, i32, i32, vp, vp,
+    lib.apex_decode_plan_host.argtypes = [vp, i32, i32, i32, i32, i32, vp,
                                           ctypes.POINTER(i64), ctypes.POINTER(i64),
                                           ctypes.POINTER(i64)]
     lib.apex_decode_last_error.restype = ctypes.c_char_p
@@ -163,11 +171,12 @@ def decode_attention(q, k_cache, v_cache, block_table, context_lens, scale, out=
 
 
 def decode_attention_ex(q, k_cache, v_cache, block_table, context_lens, scale, out=None,
-                        block_table_stride=0, num_splits=0, items_per_cu=0, workspace=None,
+                        block_table_stride=0, num_workers=0, workspace=None,
                         lse_out=None, events=None, stream=None):
     """apex_decode_attention_ex over torch tensors; returns ``out``.
 
-    ``workspace`` is an optional uint8 device tensor (caller-owned);
+    ``workspace`` is an optional uint8 device tensor (caller-owned; its first
+    counter_bytes(B, Hkv) bytes must be zero, e.g. from torch.zeros);
     ``events`` an optional pair of torch.cuda.Event recorded around the
     attention kernel."""
     import torch
@@ -182,8 +191,7 @@ def decode_attention_ex(q, k_cache, v_cache, block_table, context_lens, scale, o
     s = _stream_obj(stream, q.device)
     a.stream = int(s.cuda_stream)
     a.block_table_stride = int(block_table_stride)
-    a.num_splits = int(num_splits)
-    a.items_per_cu = int(items_per_cu)
+    a.num_workers = int(num_workers)
     if workspace is not None:
         a.workspace = _addr(workspace)
         a.workspace_bytes = workspace.numel() * workspace.element_size()
@@ -195,25 +203,26 @@ def decode_attention_ex(q, k_cache, v_cache, block_table, context_lens, scale, o
     return out
 
 
-def workspace_bytes(B, Hq, Hkv, d=128, block_size=16, num_splits=0, items_per_cu=0):
-    return int(load_library().apex_decode_workspace_bytes(B, Hq, Hkv, d, block_size,
-                                                          num_splits, items_per_cu))
+def workspace_bytes(B, Hq, Hkv, d=128, block_size=16, num_workers=0):
+    return int(load_library().apex_decode_workspace_bytes(B, Hq, Hkv, d, block_size, num_workers))
 
 
-def plan_host(context_lens, Hkv, num_cu, block_size=16, num_splits=0, items_per_cu=0):
-    """Host mirror of the split-K policy (no GPU).  Returns a dict with
-    per-request 'splits' and 'blocks_per_split' (numpy int32) and the scalars
-    'chunk', 'items' and 'partial_slots'."""
+def counter_bytes(B, Hkv):
+    return int(load_library().apex_decode_counter_bytes(B, Hkv))
+
+
+def plan_host(context_lens, Hkv, launched_workers, block_size=16, forced=False):
+    """Host mirror of the work partition (no GPU).  Returns a dict with
+    'contributors' (numpy int32 [B][Hkv]: work groups sharing each pair) and
+    the scalars 'units', 'active' and 'partials'."""
     import numpy as np
     lens = np.ascontiguousarray(np.asarray(context_lens), dtype=np.int32)
     B = lens.shape[0]
-    splits = np.zeros(max(B, 1), dtype=np.int32)
-    per = np.zeros(max(B, 1), dtype=np.int32)
-    chunk, items, slots = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    contrib = np.zeros(max(B * Hkv, 1), dtype=np.int32)
+    units, active, partials = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
     rc = load_library().apex_decode_plan_host(
-        lens.ctypes.data if B else None, B, Hkv, block_size, num_cu, num_splits, items_per_cu,
-        splits.ctypes.data, per.ctypes.data, ctypes.byref(chunk), ctypes.byref(items),
-        ctypes.byref(slots))
+        lens.ctypes.data if B else None, B, Hkv, block_size, launched_workers, int(bool(forced)),
+        contrib.ctypes.data, ctypes.byref(units), ctypes.byref(active), ctypes.byref(partials))
     _check(rc)
-    return {"splits": splits[:B], "blocks_per_split": per[:B], "chunk": chunk.value,
-            "items": items.value, "partial_slots": slots.value}
+    return {"contributors": contrib[:B * Hkv].reshape(B, Hkv), "units": units.value,
+            "active": active.value, "partials": partials.value}

@@ -8,6 +8,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libapex_decode.so")
 SOURCES = [os.path.join(CSRC, "apex_decode.hip")]
+PROBE_LIB = os.path.join(HERE, "libapex_hbm_probe.so")
+PROBE_SOURCES = [os.path.join(CSRC, "hbm_probe.hip")]
 HEADERS = [os.path.join(ROOT, "include", "apex_decode.h"),
            os.path.join(CSRC, "kernels.h"), os.path.join(CSRC, "plan_policy.h")]
 
@@ -20,14 +22,20 @@ HIPCC_FLAGS = [
 ]
 
 
-def build(out=LIB, extra=(), quiet=False):
+def _compile(sources, out, extra, quiet):
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    cmd = [hipcc, *HIPCC_FLAGS, *extra, *SOURCES, "-o", out + ".tmp"]
+    cmd = [hipcc, *HIPCC_FLAGS, *extra, *sources, "-o", out + ".tmp"]
     if not quiet:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
     os.replace(out + ".tmp", out)
     return out
+
+
+def build(out=LIB, extra=(), quiet=False):
+    """Compile the decode-attention library and the HBM probe library."""
+    _compile(PROBE_SOURCES, PROBE_LIB, extra, quiet)
+    return _compile(SOURCES, out, extra, quiet)
 
 
 if __name__ == "__main__":

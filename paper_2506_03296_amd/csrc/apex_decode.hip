@@ -1,10 +1,10 @@
 // apex_decode.hip -- host side of the C ABI declared in include/apex_decode.h.
 //
-// Validates arguments, finds or grows the per-device workspace, and enqueues
-// the planner, attention and combine kernels on the caller's stream.  No host
-// synchronisation happens on the call path (the workspace only grows when a
-// call needs more than any earlier call on that device, and growing waits for
-// the device before the old buffer is freed).
+// Validates arguments, finds or grows the per-device workspaces, and enqueues
+// the single persistent attention kernel on the caller's stream.  No host
+// synchronisation happens on the call path (a library workspace only grows
+// when a call needs more than any earlier call on that device, and growing
+// waits for the device before the old buffer is freed).
 #include <hip/hip_runtime.h>
 
 #include <mutex>
@@ -30,11 +30,19 @@ int fail(int code, const char* fmt, ...)
 }
 
 constexpr int kMaxDevices = 64;
+constexpr int kGroupKinds = 4;   // G = 1, 2, 4, 8
+constexpr int kMaxWorkers = 1 << 20;
+
+struct Buffer {
+    void* ptr = nullptr;
+    size_t bytes = 0;
+};
 
 struct DeviceState {
     int num_cu = 0;
-    void* ws = nullptr;
-    size_t ws_bytes = 0;
+    int resident[kGroupKinds] = {0, 0, 0, 0};   // work groups per CU, per G
+    Buffer counters;   // zeroed at allocation; calls leave it zero
+    Buffer partials;
 };
 
 std::mutex g_mutex;
@@ -42,67 +50,81 @@ DeviceState g_dev[kMaxDevices];
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-struct WsLayout {
-    size_t hdr, req, items, pacc, pml, total;
-};
+int group_index(int G) { return G == 1 ? 0 : G == 2 ? 1 : G == 4 ? 2 : 3; }
 
-WsLayout ws_layout(int B, int G, int64_t max_items)
+size_t counter_bytes(int B, int Hkv) { return align_up((size_t)B * Hkv * sizeof(int32_t), 256); }
+
+size_t partial_bytes(int64_t workers, int G)
 {
-    WsLayout w;
-    size_t off = 0;
-    w.hdr = off;
-    off = align_up(off + sizeof(apex::WsHeader), 256);
-    w.req = off;
-    off = align_up(off + sizeof(apex::ReqInfo) * (size_t)(B > 0 ? B : 1), 256);
-    w.items = off;
-    off = align_up(off + sizeof(apex::Item) * (size_t)max_items, 256);
-    w.pacc = off;
-    off = align_up(off + sizeof(float) * (size_t)max_items * G * apex::kHeadDim, 256);
-    w.pml = off;
-    off = align_up(off + sizeof(float) * 2 * (size_t)max_items * G, 256);
-    w.total = off;
-    return w;
+    return align_up(sizeof(float) * 2 * (size_t)workers * G * apex::kHeadDim, 256) +
+           align_up(sizeof(float) * 2 * 2 * (size_t)workers * G, 256);
 }
 
-int device_cu_count(int dev, int* num_cu)
+int resident_groups(int G, int* out)
+{
+    int n = 0;
+    hipError_t e;
+    switch (G) {
+        case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<1>, apex::kAttnThreads, 0); break;
+        case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<2>, apex::kAttnThreads, 0); break;
+        case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<4>, apex::kAttnThreads, 0); break;
+        default: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<8>, apex::kAttnThreads, 0); break;
+    }
+    if (e != hipSuccess || n <= 0)
+        return fail(APEX_ERR_HIP, "occupancy query failed: %s", hipGetErrorString(e));
+    *out = n;
+    return APEX_OK;
+}
+
+// Default persistent grid for group size G on device dev: CUs x resident groups.
+int default_workers(int dev, int G, int64_t* out)
 {
     if (dev < 0 || dev >= kMaxDevices) return fail(APEX_ERR_HIP, "device ordinal %d out of range", dev);
     std::lock_guard<std::mutex> lock(g_mutex);
-    if (g_dev[dev].num_cu == 0) {
+    DeviceState& s = g_dev[dev];
+    if (s.num_cu == 0) {
         int n = 0;
         hipError_t e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
         if (e != hipSuccess || n <= 0)
             return fail(APEX_ERR_HIP, "hipDeviceGetAttribute(CU count): %s", hipGetErrorString(e));
-        g_dev[dev].num_cu = n;
+        s.num_cu = n;
     }
-    *num_cu = g_dev[dev].num_cu;
+    const int gi = group_index(G);
+    if (s.resident[gi] == 0) {
+        int rc = resident_groups(G, &s.resident[gi]);
+        if (rc != APEX_OK) return rc;
+    }
+    *out = (int64_t)s.num_cu * s.resident[gi];
     return APEX_OK;
 }
 
-int library_workspace(int dev, size_t need, void** out)
+int grow(Buffer& buf, size_t need, bool zero)
 {
-    std::lock_guard<std::mutex> lock(g_mutex);
-    DeviceState& s = g_dev[dev];
-    if (s.ws_bytes < need) {
-        if (s.ws) {
-            hipError_t e = hipDeviceSynchronize();
-            if (e != hipSuccess) return fail(APEX_ERR_HIP, "hipDeviceSynchronize: %s", hipGetErrorString(e));
-            (void)hipFree(s.ws);
-            s.ws = nullptr;
-            s.ws_bytes = 0;
-        }
-        const size_t bytes = align_up(need + need / 4, 1 << 20);
-        void* p = nullptr;
-        hipError_t e = hipMalloc(&p, bytes);
-        if (e != hipSuccess || !p) {
-            (void)hipGetLastError();
-            return fail(APEX_ERR_OUT_OF_MEMORY, "hipMalloc(%zu) for the workspace failed: %s", bytes,
-                        hipGetErrorString(e));
-        }
-        s.ws = p;
-        s.ws_bytes = bytes;
+    if (buf.bytes >= need) return APEX_OK;
+    if (buf.ptr) {
+        hipError_t e = hipDeviceSynchronize();
+        if (e != hipSuccess) return fail(APEX_ERR_HIP, "hipDeviceSynchronize: %s", hipGetErrorString(e));
+        (void)hipFree(buf.ptr);
+        buf.ptr = nullptr;
+        buf.bytes = 0;
     }
-    *out = s.ws;
+    const size_t bytes = align_up(need + need / 4, 1 << 20);
+    void* p = nullptr;
+    hipError_t e = hipMalloc(&p, bytes);
+    if (e != hipSuccess || !p) {
+        (void)hipGetLastError();
+        return fail(APEX_ERR_OUT_OF_MEMORY, "hipMalloc(%zu) for a workspace failed: %s", bytes,
+                    hipGetErrorString(e));
+    }
+    if (zero) {
+        e = hipMemset(p, 0, bytes);
+        if (e != hipSuccess) {
+            (void)hipFree(p);
+            return fail(APEX_ERR_HIP, "hipMemset of the counters failed: %s", hipGetErrorString(e));
+        }
+    }
+    buf.ptr = p;
+    buf.bytes = bytes;
     return APEX_OK;
 }
 
@@ -129,41 +151,19 @@ int check_shapes(int B, int Hq, int Hkv, int d, int block_size)
 }
 
 template <int G>
-int launch(const apex_decode_args& a, const apex::WsPtrs& ws, int64_t target, int64_t max_items,
-           hipStream_t stream)
+int launch(const apex::AttnParams& p, int64_t workers, void* const* events, hipStream_t stream)
 {
-    apex::plan_kernel<<<1, apex::kPlanThreads, 0, stream>>>(a.context_lens, a.B, a.Hkv, target,
-                                                            a.num_splits, ws);
-    apex::AttnParams p;
-    p.q = (const apex::f16*)a.q;
-    p.k = (const apex::f16*)a.k_cache;
-    p.v = (const apex::f16*)a.v_cache;
-    p.bt = a.block_table;
-    p.out = (apex::f16*)a.out;
-    p.lse = a.lse_out;
-    p.bt_stride = a.block_table_stride;
-    p.ws = ws;
-    p.scale_log2 = a.scale * 1.4426950408889634f;
-    p.Hq = a.Hq;
-    p.Hkv = a.Hkv;
-    if (a.attn_kernel_events[0]) {
-        hipError_t e = hipEventRecord((hipEvent_t)a.attn_kernel_events[0], stream);
+    if (events[0]) {
+        hipError_t e = hipEventRecord((hipEvent_t)events[0], stream);
         if (e != hipSuccess) return fail(APEX_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
     }
-    apex::attn_kernel<G><<<(unsigned)max_items, apex::kAttnThreads, 0, stream>>>(p);
-    if (a.attn_kernel_events[1]) {
-        hipError_t e = hipEventRecord((hipEvent_t)a.attn_kernel_events[1], stream);
-        if (e != hipSuccess) return fail(APEX_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
-    }
-    apex::CombineParams cp;
-    cp.out = (apex::f16*)a.out;
-    cp.lse = a.lse_out;
-    cp.ws = ws;
-    cp.Hq = a.Hq;
-    cp.Hkv = a.Hkv;
-    apex::combine_kernel<G><<<(unsigned)((int64_t)a.B * a.Hkv), apex::kAttnThreads, 0, stream>>>(cp);
+    apex::attn_kernel<G><<<(unsigned)workers, apex::kAttnThreads, 0, stream>>>(p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(APEX_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+    if (events[1]) {
+        e = hipEventRecord((hipEvent_t)events[1], stream);
+        if (e != hipSuccess) return fail(APEX_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    }
     return APEX_OK;
 }
 
@@ -171,48 +171,60 @@ int launch(const apex_decode_args& a, const apex::WsPtrs& ws, int64_t target, in
 
 extern "C" {
 
-int apex_decode_version(void) { return 100; }
+int apex_decode_version(void) { return 200; }
 
 const char* apex_decode_last_error(void) { return g_last_error; }
 
-size_t apex_decode_workspace_bytes(int B, int Hq, int Hkv, int d, int block_size, int num_splits,
-                                   int items_per_cu)
+size_t apex_decode_counter_bytes(int B, int Hkv)
 {
-    if (check_shapes(B, Hq, Hkv, d, block_size) != APEX_OK || num_splits < 0 || items_per_cu < 0)
-        return 0;
-    int dev = 0, num_cu = 0;
-    if (hipGetDevice(&dev) != hipSuccess || device_cu_count(dev, &num_cu) != APEX_OK) return 0;
-    const int64_t mi = apex::max_items(B, Hkv, num_cu, items_per_cu, num_splits);
-    return ws_layout(B, Hq / Hkv, mi).total;
+    if (B < 0 || Hkv <= 0) return 0;
+    return counter_bytes(B, Hkv);
 }
 
-int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block_size, int num_cu,
-                          int num_splits, int items_per_cu, int32_t* splits_out,
-                          int32_t* blocks_per_split_out, int64_t* chunk_out, int64_t* items_out,
-                          int64_t* partial_slots_out)
+size_t apex_decode_workspace_bytes(int B, int Hq, int Hkv, int d, int block_size, int num_workers)
+{
+    if (check_shapes(B, Hq, Hkv, d, block_size) != APEX_OK || num_workers < 0) return 0;
+    int64_t workers = num_workers;
+    if (workers == 0) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess || default_workers(dev, Hq / Hkv, &workers) != APEX_OK)
+            return 0;
+    }
+    return counter_bytes(B, Hkv) + partial_bytes(workers, Hq / Hkv);
+}
+
+int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block_size,
+                          int launched_workers, int forced, int32_t* contributors_out,
+                          int64_t* units_out, int64_t* active_out, int64_t* partials_out)
 {
     g_last_error[0] = 0;
-    if (B < 0 || Hkv <= 0 || num_cu <= 0 || num_splits < 0 || items_per_cu < 0)
-        return fail(APEX_ERR_INVALID_ARG, "bad planner arguments");
+    if (B < 0 || Hkv <= 0 || launched_workers <= 0)
+        return fail(APEX_ERR_INVALID_ARG, "bad partition arguments");
     if (B > 0 && !context_lens) return fail(APEX_ERR_INVALID_ARG, "context_lens is NULL");
     if (block_size != apex::kBlockSize)
         return fail(APEX_ERR_UNSUPPORTED, "block_size %d unsupported (only 16)", block_size);
-    int64_t units = 0;
-    for (int b = 0; b < B; ++b) units += apex::blocks_of(context_lens[b], block_size);
-    units *= Hkv;
-    const int64_t chunk = apex::chunk_blocks(units, apex::target_items(num_cu, items_per_cu));
-    int64_t items = 0, slots = 0;
+    int64_t blocks = 0;
+    for (int b = 0; b < B; ++b) blocks += apex::blocks_of(context_lens[b], block_size);
+    const int64_t units = blocks * Hkv;
+    const int64_t W = apex::active_workers(units, launched_workers,
+                                           forced ? 1 : apex::kMinUnitsPerWorker);
+    int64_t partials = 0, pre = 0;
     for (int b = 0; b < B; ++b) {
-        const apex::SplitPlan sp =
-            apex::split_request(apex::blocks_of(context_lens[b], block_size), chunk, num_splits);
-        if (splits_out) splits_out[b] = sp.n;
-        if (blocks_per_split_out) blocks_per_split_out[b] = sp.per;
-        items += (int64_t)sp.n * Hkv;
-        if (sp.n > 1) slots += (int64_t)sp.n * Hkv;
+        const int64_t nb = apex::blocks_of(context_lens[b], block_size);
+        for (int g = 0; g < Hkv; ++g) {
+            int64_t n = 0;
+            if (nb > 0) {
+                const int64_t p0 = pre * Hkv + (int64_t)g * nb;
+                n = apex::worker_of(p0 + nb - 1, units, W) - apex::worker_of(p0, units, W) + 1;
+                if (n > 1) partials += n;
+            }
+            if (contributors_out) contributors_out[(size_t)b * Hkv + g] = (int32_t)n;
+        }
+        pre += nb;
     }
-    if (chunk_out) *chunk_out = chunk;
-    if (items_out) *items_out = items;
-    if (partial_slots_out) *partial_slots_out = slots;
+    if (units_out) *units_out = units;
+    if (active_out) *active_out = units > 0 ? W : 0;
+    if (partials_out) *partials_out = partials;
     return APEX_OK;
 }
 
@@ -224,8 +236,8 @@ int apex_decode_attention_ex(const apex_decode_args* args)
     int rc = check_shapes(a.B, a.Hq, a.Hkv, a.d, a.block_size);
     if (rc != APEX_OK) return rc;
     if (a.flags != 0) return fail(APEX_ERR_INVALID_ARG, "flags must be 0");
-    if (a.num_splits < 0) return fail(APEX_ERR_INVALID_ARG, "num_splits = %d is negative", a.num_splits);
-    if (a.items_per_cu < 0) return fail(APEX_ERR_INVALID_ARG, "items_per_cu is negative");
+    if (a.num_workers < 0 || a.num_workers > kMaxWorkers)
+        return fail(APEX_ERR_INVALID_ARG, "num_workers = %d out of range", a.num_workers);
     if (a.block_table_stride < 0) return fail(APEX_ERR_INVALID_ARG, "block_table_stride is negative");
     if (a.B == 0) return APEX_OK;
     if (!a.q || !a.k_cache || !a.v_cache || !a.block_table || !a.context_lens || !a.out)
@@ -245,39 +257,60 @@ int apex_decode_attention_ex(const apex_decode_args* args)
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return fail(APEX_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
-    int num_cu = 0;
-    rc = device_cu_count(dev, &num_cu);
-    if (rc != APEX_OK) return rc;
-
     const int G = a.Hq / a.Hkv;
-    const int64_t target = apex::target_items(num_cu, a.items_per_cu);
-    const int64_t mi = apex::max_items(a.B, a.Hkv, num_cu, a.items_per_cu, a.num_splits);
-    if (mi > 0x7fffffff) return fail(APEX_ERR_UNSUPPORTED, "too many work items (%lld)", (long long)mi);
-    const WsLayout lay = ws_layout(a.B, G, mi);
-    void* ws = a.workspace;
-    if (ws) {
-        if (a.workspace_bytes < lay.total)
-            return fail(APEX_ERR_OUT_OF_MEMORY, "caller workspace holds %zu bytes, %zu needed",
-                        a.workspace_bytes, lay.total);
-        if (!aligned(ws, 256)) return fail(APEX_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
-    } else {
-        rc = library_workspace(dev, lay.total, &ws);
+    int64_t workers = a.num_workers;
+    if (workers == 0) {
+        rc = default_workers(dev, G, &workers);
         if (rc != APEX_OK) return rc;
     }
-    apex::WsPtrs wp;
-    char* base = (char*)ws;
-    wp.hdr = (apex::WsHeader*)(base + lay.hdr);
-    wp.req = (apex::ReqInfo*)(base + lay.req);
-    wp.items = (apex::Item*)(base + lay.items);
-    wp.pacc = (float*)(base + lay.pacc);
-    wp.pml = (float*)(base + lay.pml);
+
+    const size_t cbytes = counter_bytes(a.B, a.Hkv);
+    const size_t pbytes = partial_bytes(workers, G);
+    void* counters = nullptr;
+    void* partials = nullptr;
+    if (a.workspace) {
+        if (a.workspace_bytes < cbytes + pbytes)
+            return fail(APEX_ERR_OUT_OF_MEMORY, "caller workspace holds %zu bytes, %zu needed",
+                        a.workspace_bytes, cbytes + pbytes);
+        if (!aligned(a.workspace, 256)) return fail(APEX_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+        counters = a.workspace;
+        partials = (char*)a.workspace + cbytes;
+    } else {
+        std::lock_guard<std::mutex> lock(g_mutex);
+        DeviceState& s = g_dev[dev];
+        rc = grow(s.counters, cbytes, true);
+        if (rc != APEX_OK) return rc;
+        rc = grow(s.partials, pbytes, false);
+        if (rc != APEX_OK) return rc;
+        counters = s.counters.ptr;
+        partials = s.partials.ptr;
+    }
+
+    apex::AttnParams p;
+    p.q = (const apex::f16*)a.q;
+    p.k = (const apex::f16*)a.k_cache;
+    p.v = (const apex::f16*)a.v_cache;
+    p.bt = a.block_table;
+    p.lens = a.context_lens;
+    p.out = (apex::f16*)a.out;
+    p.lse = a.lse_out;
+    p.counters = (int32_t*)counters;
+    p.pacc = (float*)partials;
+    p.pml = (float*)((char*)partials +
+                     align_up(sizeof(float) * 2 * (size_t)workers * G * apex::kHeadDim, 256));
+    p.bt_stride = a.block_table_stride;
+    p.scale_log2 = a.scale * 1.4426950408889634f;
+    p.B = a.B;
+    p.Hq = a.Hq;
+    p.Hkv = a.Hkv;
+    p.min_units = a.num_workers > 0 ? 1 : apex::kMinUnitsPerWorker;
 
     hipStream_t stream = (hipStream_t)a.stream;
     switch (G) {
-        case 1: return launch<1>(a, wp, target, mi, stream);
-        case 2: return launch<2>(a, wp, target, mi, stream);
-        case 4: return launch<4>(a, wp, target, mi, stream);
-        default: return launch<8>(a, wp, target, mi, stream);
+        case 1: return launch<1>(p, workers, a.attn_kernel_events, stream);
+        case 2: return launch<2>(p, workers, a.attn_kernel_events, stream);
+        case 4: return launch<4>(p, workers, a.attn_kernel_events, stream);
+        default: return launch<8>(p, workers, a.attn_kernel_events, stream);
     }
 }
 
@@ -309,15 +342,17 @@ int apex_decode_release_workspace(void)
     std::lock_guard<std::mutex> lock(g_mutex);
     int rc = APEX_OK;
     for (int d = 0; d < kMaxDevices; ++d) {
-        if (!g_dev[d].ws) continue;
+        DeviceState& s = g_dev[d];
+        if (!s.counters.ptr && !s.partials.ptr) continue;
         int prev = 0;
         (void)hipGetDevice(&prev);
         if (hipSetDevice(d) == hipSuccess && hipDeviceSynchronize() == hipSuccess) {
-            (void)hipFree(g_dev[d].ws);
-            g_dev[d].ws = nullptr;
-            g_dev[d].ws_bytes = 0;
+            if (s.counters.ptr) (void)hipFree(s.counters.ptr);
+            if (s.partials.ptr) (void)hipFree(s.partials.ptr);
+            s.counters = Buffer();
+            s.partials = Buffer();
         } else {
-            rc = fail(APEX_ERR_HIP, "could not release the workspace of device %d", d);
+            rc = fail(APEX_ERR_HIP, "could not release the workspaces of device %d", d);
         }
         (void)hipSetDevice(prev);
     }

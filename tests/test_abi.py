@@ -64,73 +64,87 @@ def test_args_struct_matches_header_field_order():
 
 
 # ---------------------------------------------------------------------------
-# split-K planner policy (host mirror)
+# work partition (host mirror) against a brute-force assignment of units
 # ---------------------------------------------------------------------------
 
-def _check_plan(lens, Hkv, num_cu, num_splits=0, items_per_cu=0):
-    p = A.plan_host(lens, Hkv, num_cu, num_splits=num_splits, items_per_cu=items_per_cu)
-    lens = np.asarray(lens, dtype=np.int64)
-    blocks = np.where(lens > 0, -(-lens // 16), 0)
-    n, per, chunk = p["splits"], p["blocks_per_split"], p["chunk"]
-    assert chunk >= 8
-    target = num_cu * (items_per_cu or 16)
-    assert chunk >= -(-int(blocks.sum() * Hkv) // target)
-    for b in range(len(lens)):
-        if blocks[b] == 0:
-            assert n[b] == 1 and per[b] == 0
-            continue
-        assert n[b] * per[b] >= blocks[b]           # every block covered
-        assert (-(-blocks[b] // per[b])) <= n[b]
-        if num_splits:
-            assert n[b] == num_splits
-        else:
-            assert per[b] <= chunk
-            assert (n[b] == 1) == (blocks[b] <= chunk)
-            assert (n[b] - 1) * per[b] < blocks[b]   # no empty range
-    assert p["items"] == int(n.sum()) * Hkv
-    assert p["partial_slots"] == int(n[n > 1].sum()) * Hkv
-    if not num_splits:
-        assert p["items"] <= target + len(lens) * Hkv
+def _brute_partition(lens, Hkv, launched, forced):
+    blocks = [(-(-int(L) // 16)) if L > 0 else 0 for L in lens]
+    U = sum(blocks) * Hkv
+    W = min(launched, max(1, U // (1 if forced else 8)))
+    owner = []
+    starts = [w * U // W for w in range(W + 1)]
+    for w in range(W):
+        owner += [w] * (starts[w + 1] - starts[w])
+    assert len(owner) == U
+    contrib = np.zeros((len(lens), Hkv), dtype=np.int64)
+    per_worker_partials = np.zeros(W, dtype=np.int64)
+    u = 0
+    for b, nb in enumerate(blocks):
+        for g in range(Hkv):
+            ws = sorted(set(owner[u:u + nb]))
+            contrib[b, g] = len(ws)
+            if len(ws) > 1:
+                for w in ws:
+                    per_worker_partials[w] += 1
+            u += nb
+    return U, W, contrib, per_worker_partials
+
+
+def _check_plan(lens, Hkv, launched, forced=False):
+    p = A.plan_host(lens, Hkv, launched, forced=forced)
+    U, W, contrib, pwp = _brute_partition(lens, Hkv, launched, forced)
+    assert p["units"] == U
+    assert p["active"] == (W if U else 0)
+    assert np.array_equal(p["contributors"], contrib)
+    assert p["partials"] == int(contrib[contrib > 1].sum())
+    assert np.all(pwp <= 2)          # a worker has at most two partial segments
     return p
 
 
 @pytest.mark.parametrize("seed", range(6))
-def test_plan_random_batches(lib, seed):
+def test_partition_random_batches(lib, seed):
     rng = np.random.default_rng(seed)
-    B = int(rng.integers(1, 700))
-    lens = rng.integers(-3, 40000, size=B)
+    B = int(rng.integers(1, 300))
+    lens = rng.integers(-3, 5000, size=B)
     lens[rng.random(B) < 0.1] = 0
-    _check_plan(lens, int(rng.choice([1, 2, 8, 32])), int(rng.choice([1, 80, 256])))
+    Hkv = int(rng.choice([1, 2, 8, 32]))
+    _check_plan(lens, Hkv, int(rng.choice([1, 7, 80, 1024])))
+    _check_plan(lens, Hkv, int(rng.choice([1, 3, 64, 100000])), forced=True)
 
 
-def test_plan_edge_lengths(lib):
+def test_partition_edge_lengths(lib):
     for L in (0, 1, 15, 16, 17, 31, 32, 33, 16 * 8, 16 * 8 + 1, 32768):
-        _check_plan([L], 8, 256)
-    p = _check_plan([], 8, 256)
-    assert p["items"] == 0
+        _check_plan([L], 8, 1024)
+        _check_plan([L], 8, 5, forced=True)
+    p = _check_plan([], 8, 1024)
+    assert p["units"] == 0 and p["active"] == 0
+    p = _check_plan([0, 0, -1], 8, 1024)
+    assert p["units"] == 0
 
 
-@pytest.mark.parametrize("n", [1, 2, 7, 64])
-def test_plan_forced_splits(lib, n):
-    p = _check_plan([17, 64, 200, 511, 0], 32, 256, num_splits=n)
-    assert list(p["splits"]) == [n, n, n, n, 1]
+def test_partition_one_worker_writes_everything_directly(lib):
+    p = _check_plan([17, 64, 200, 511, 0], 32, 1, forced=True)
+    assert p["partials"] == 0
+    assert np.all(p["contributors"][:4] == 1)
 
 
-def test_plan_short_requests_stay_whole_long_ones_split(lib):
-    lens = [300] * 256 + [16000] * 256
-    p = _check_plan(lens, 8, 256)
-    assert np.all(p["splits"][:256] == 1) and np.all(p["splits"][256:] > 1)
+def test_partition_one_unit_per_worker_splits_every_multi_block_pair(lib):
+    lens = [17, 64, 200, 511]
+    p = _check_plan(lens, 4, 10 ** 6, forced=True)
+    blocks = [-(-L // 16) for L in lens]
+    for b, nb in enumerate(blocks):
+        assert np.all(p["contributors"][b] == nb)
 
 
-def test_plan_named_workload_partial_traffic_is_small(lib):
+def test_partition_named_workloads_partial_traffic_is_small(lib):
     import apex_workloads as W
     for name in ("c2", "c3", "c4", "c5"):
         cfg = W.CONFIGS[name]
         lay, _ = W.config_layout(cfg)
-        p = _check_plan(lay.lens, cfg.Hkv, 256)
+        p = _check_plan(lay.lens, cfg.Hkv, 1024)
         G = cfg.Hq // cfg.Hkv
-        partial_bytes = 2 * p["partial_slots"] * G * (128 + 2) * 4
-        assert partial_bytes < 0.03 * W.algorithmic_bytes(lay.lens, cfg.B, cfg.Hq, cfg.Hkv, 128)
+        partial_bytes = 2 * p["partials"] * G * (128 + 2) * 4
+        assert partial_bytes < 0.01 * W.algorithmic_bytes(lay.lens, cfg.B, cfg.Hq, cfg.Hkv, 128)
 
 
 # ---------------------------------------------------------------------------
@@ -172,7 +186,7 @@ def test_empty_batch_is_a_noop(lib):
 
 
 def test_ex_rejects_flags_and_negative_fields(lib):
-    for field, value in (("flags", 1), ("num_splits", -1), ("items_per_cu", -2),
+    for field, value in (("flags", 1), ("num_workers", -1), ("num_workers", 1 << 21),
                          ("block_table_stride", -5)):
         a = A.DecodeArgs()
         a.q, a.k_cache, a.v_cache = FAKE, FAKE + (1 << 30), FAKE + (2 << 30)
@@ -190,3 +204,8 @@ def test_plan_host_rejects_bad_arguments(lib):
         A.plan_host([5], 8, 0)
     with pytest.raises(A.ApexError):
         A.plan_host([5], 8, 256, block_size=32)
+
+
+def test_counter_bytes(lib):
+    assert A.counter_bytes(512, 8) == 512 * 8 * 4
+    assert A.counter_bytes(3, 1) == 256

@@ -89,13 +89,13 @@ SMALL = [
 
 
 @pytest.mark.parametrize("name,lens,Hq,Hkv", SMALL, ids=[s[0] for s in SMALL])
-@pytest.mark.parametrize("splits", [0, 1, 2, 7, 64])
-def test_small_cases_with_poison(torch_cuda, apex, oracle_mod, name, lens, Hq, Hkv, splits):
+@pytest.mark.parametrize("workers", [0, 1, 2, 7, 64, 100000])
+def test_small_cases_with_poison(torch_cuda, apex, oracle_mod, name, lens, Hq, Hkv, workers):
     case = W.make_host_case(lens, Hq, Hkv, seed=len(lens) * 31 + Hq, poison=True)
     ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
                                           case.context_lens, case.scale)
-    got = run_gpu(torch_cuda, apex, case, num_splits=splits)
-    assert_parity(got, ref, f"{name} splits={splits}")
+    got = run_gpu(torch_cuda, apex, case, num_workers=workers)
+    assert_parity(got, ref, f"{name} workers={workers}")
     for b, L in enumerate(lens):
         if L == 0:
             assert np.all(got[b] == 0)
@@ -107,9 +107,9 @@ def test_lse_output(torch_cuda, apex, oracle_mod):
     _, lse_ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache,
                                                  case.block_table, case.context_lens, case.scale,
                                                  return_lse=True)
-    for splits in (0, 1, 5):
+    for workers in (0, 1, 5, 3000):
         lse = torch.empty((4, 16), dtype=torch.float32, device="cuda")
-        run_gpu(torch, apex, case, num_splits=splits, lse_out=lse)
+        run_gpu(torch, apex, case, num_workers=workers, lse_out=lse)
         got = lse.cpu().numpy().astype(np.float64)
         assert np.all(np.isneginf(got[2]))
         fin = np.isfinite(lse_ref)
@@ -131,13 +131,22 @@ def test_caller_workspace_and_side_stream(torch_cuda, apex, oracle_mod):
                                           case.context_lens, case.scale)
     q, k, v, bt, lens = to_dev(torch, case)
     nbytes = apex.workspace_bytes(3, 32, 8)
-    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
         out = apex.decode_attention_ex(q, k, v, bt, lens, case.scale, workspace=ws, stream=s)
     s.synchronize()
     assert_parity(out.cpu().numpy(), ref, "caller workspace, side stream")
+    cb = apex.counter_bytes(3, 8)
+    assert int(ws[:cb].abs().sum()) == 0          # counters left at zero
+    # a forced small grid shares pairs between work groups; counters still return to zero
+    ws2 = torch.zeros(apex.workspace_bytes(3, 32, 8, num_workers=40), dtype=torch.uint8, device="cuda")
+    for _ in range(3):
+        out = apex.decode_attention_ex(q, k, v, bt, lens, case.scale, workspace=ws2, num_workers=40)
+        torch.cuda.synchronize()
+        assert_parity(out.cpu().numpy(), ref, "caller workspace, 40 workers")
+        assert int(ws2[:cb].abs().sum()) == 0
     small = torch.empty(256, dtype=torch.uint8, device="cuda")
     with pytest.raises(apex.ApexError) as e:
         apex.decode_attention_ex(q, k, v, bt, lens, case.scale, workspace=small)
@@ -172,8 +181,8 @@ def test_identical_keys_give_mean_of_v(torch_cuda, apex):
 def test_unit_values_give_unit_output(torch_cuda, apex):
     case = W.make_host_case([1, 50, 5000], 32, 8, seed=10)
     case.v_cache[:] = 1
-    for splits in (0, 3):
-        got = run_gpu(torch_cuda, apex, case, num_splits=splits)
+    for workers in (0, 3, 777):
+        got = run_gpu(torch_cuda, apex, case, num_workers=workers)
         assert np.all(got == 1.0)
 
 
@@ -207,8 +216,8 @@ def test_late_peaked_key_dominates(torch_cuda, apex, oracle_mod):
     case.k_cache[blk, 0, t % 16] = (40.0 * q / np.linalg.norm(q)).astype(np.float16)
     ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
                                           case.context_lens, case.scale)
-    for splits in (0, 1, 9):
-        assert_parity(run_gpu(torch_cuda, apex, case, num_splits=splits), ref, f"peaked splits={splits}")
+    for workers in (0, 1, 9, 250):
+        assert_parity(run_gpu(torch_cuda, apex, case, num_workers=workers), ref, f"peaked workers={workers}")
 
 
 def test_repeated_runs_are_bitwise_identical(torch_cuda, apex):
