@@ -22,16 +22,19 @@ extern "C" {
 #endif
 
 /* Reads `bytes` (a multiple of 16) of `buf` once with 128-bit loads using
- * `blocks` work groups of 256 threads (0 = 8 per compute unit).  `sink` is a
- * 4-byte device word the kernel writes only if the data XOR to a sentinel. */
-int apex_hbm_probe_stream(const void* buf, size_t bytes, int blocks, uint32_t* sink, void* stream);
+ * `blocks` work groups of 256 threads (0 = 8 per compute unit).  flags bit 0
+ * = non-temporal loads.  `sink` is a 4-byte device word the kernel writes
+ * only if the data XOR to a sentinel. */
+int apex_hbm_probe_stream(const void* buf, size_t bytes, int blocks, int flags, uint32_t* sink,
+                          void* stream);
 
 /* Reads `n_chunks` chunks of 4096 bytes, chunk i starting at byte
- * chunk_ids[i] * 4096 of `buf` (int32 ids, device memory), one 64-lane wave
+ * chunk_ids[i] * 4096 of `buf` (int32 ids, device memory), a 64-lane wave
  * per chunk with 128-bit loads, `blocks` work groups of 256 threads
- * (0 = 8 per compute unit). */
+ * (0 = 8 per compute unit).  flags bit 0 = non-temporal loads, bits 1-3 =
+ * chunks each wave has in flight (1, 2 or 4). */
 int apex_hbm_probe_gather(const void* buf, const int32_t* chunk_ids, int64_t n_chunks, int blocks,
-                          uint32_t* sink, void* stream);
+                          int flags, uint32_t* sink, void* stream);
 
 #ifdef __cplusplus
 }

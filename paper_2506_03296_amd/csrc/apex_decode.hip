@@ -151,13 +151,14 @@ int check_shapes(int B, int Hq, int Hkv, int d, int block_size)
 }
 
 template <int G>
-int launch(const apex::AttnParams& p, int64_t workers, void* const* events, hipStream_t stream)
+int launch(const apex::AttnParams& p, const int32_t* bt, const int32_t* lens, int64_t workers,
+           void* const* events, hipStream_t stream)
 {
     if (events[0]) {
         hipError_t e = hipEventRecord((hipEvent_t)events[0], stream);
         if (e != hipSuccess) return fail(APEX_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
     }
-    apex::attn_kernel<G><<<(unsigned)workers, apex::kAttnThreads, 0, stream>>>(p);
+    apex::attn_kernel<G><<<(unsigned)workers, apex::kAttnThreads, 0, stream>>>(p, bt, lens);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(APEX_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     if (events[1]) {
@@ -290,8 +291,6 @@ int apex_decode_attention_ex(const apex_decode_args* args)
     p.q = (const apex::f16*)a.q;
     p.k = (const apex::f16*)a.k_cache;
     p.v = (const apex::f16*)a.v_cache;
-    p.bt = a.block_table;
-    p.lens = a.context_lens;
     p.out = (apex::f16*)a.out;
     p.lse = a.lse_out;
     p.counters = (int32_t*)counters;
@@ -307,10 +306,10 @@ int apex_decode_attention_ex(const apex_decode_args* args)
 
     hipStream_t stream = (hipStream_t)a.stream;
     switch (G) {
-        case 1: return launch<1>(p, workers, a.attn_kernel_events, stream);
-        case 2: return launch<2>(p, workers, a.attn_kernel_events, stream);
-        case 4: return launch<4>(p, workers, a.attn_kernel_events, stream);
-        default: return launch<8>(p, workers, a.attn_kernel_events, stream);
+        case 1: return launch<1>(p, a.block_table, a.context_lens, workers, a.attn_kernel_events, stream);
+        case 2: return launch<2>(p, a.block_table, a.context_lens, workers, a.attn_kernel_events, stream);
+        case 4: return launch<4>(p, a.block_table, a.context_lens, workers, a.attn_kernel_events, stream);
+        default: return launch<8>(p, a.block_table, a.context_lens, workers, a.attn_kernel_events, stream);
     }
 }
 

@@ -7,6 +7,14 @@ namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+template <bool NT>
+__device__ inline u32x4 ld(const u32x4* p)
+{
+    if constexpr (NT) return __builtin_nontemporal_load(p);
+    else return *p;
+}
+
+template <bool NT>
 __global__ __launch_bounds__(256) void stream_kernel(const u32x4* __restrict__ p, size_t n16,
                                                      uint32_t* sink)
 {
@@ -14,13 +22,16 @@ __global__ __launch_bounds__(256) void stream_kernel(const u32x4* __restrict__ p
     size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     u32x4 acc = {0u, 0u, 0u, 0u};
     for (; i + 3 * stride < n16; i += 4 * stride) {
-        const u32x4 a = p[i], b = p[i + stride], c = p[i + 2 * stride], d = p[i + 3 * stride];
+        const u32x4 a = ld<NT>(p + i), b = ld<NT>(p + i + stride), c = ld<NT>(p + i + 2 * stride),
+                    d = ld<NT>(p + i + 3 * stride);
         acc ^= a ^ b ^ c ^ d;
     }
-    for (; i < n16; i += stride) acc ^= p[i];
+    for (; i < n16; i += stride) acc ^= ld<NT>(p + i);
     if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9e3779b9u) *sink = 1u;
 }
 
+// Each wave reads U chunks of 4 KiB per step (U x 4 loads of 16 B per lane).
+template <int U, bool NT>
 __global__ __launch_bounds__(256) void gather_kernel(const u32x4* __restrict__ p,
                                                      const int32_t* __restrict__ ids,
                                                      int64_t n_chunks, uint32_t* sink)
@@ -29,16 +40,22 @@ __global__ __launch_bounds__(256) void gather_kernel(const u32x4* __restrict__ p
     const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
     int64_t w = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
     u32x4 acc = {0u, 0u, 0u, 0u};
-    for (; w + waves < n_chunks; w += 2 * waves) {
-        const u32x4* c0 = p + (size_t)ids[w] * 256 + lane;
-        const u32x4* c1 = p + (size_t)ids[w + waves] * 256 + lane;
-        const u32x4 a0 = c0[0], a1 = c0[64], a2 = c0[128], a3 = c0[192];
-        const u32x4 b0 = c1[0], b1 = c1[64], b2 = c1[128], b3 = c1[192];
-        acc ^= a0 ^ a1 ^ a2 ^ a3 ^ b0 ^ b1 ^ b2 ^ b3;
+    for (; w + (U - 1) * waves < n_chunks; w += U * waves) {
+        u32x4 r[U][4];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const u32x4* c = p + (size_t)ids[w + u * waves] * 256 + lane;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) r[u][k] = ld<NT>(c + 64 * k);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) acc ^= r[u][k];
     }
     for (; w < n_chunks; w += waves) {
-        const u32x4* c0 = p + (size_t)ids[w] * 256 + lane;
-        acc ^= c0[0] ^ c0[64] ^ c0[128] ^ c0[192];
+        const u32x4* c = p + (size_t)ids[w] * 256 + lane;
+        acc ^= ld<NT>(c) ^ ld<NT>(c + 64) ^ ld<NT>(c + 128) ^ ld<NT>(c + 192);
     }
     if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9e3779b9u) *sink = 1u;
 }
@@ -57,24 +74,40 @@ int default_blocks(int blocks)
 
 extern "C" {
 
-int apex_hbm_probe_stream(const void* buf, size_t bytes, int blocks, uint32_t* sink, void* stream)
+int apex_hbm_probe_stream(const void* buf, size_t bytes, int blocks, int flags, uint32_t* sink,
+                          void* stream)
 {
-    if (!buf || !sink || bytes % 16 || blocks < 0) return -1;
+    if (!buf || !sink || bytes % 16 || blocks < 0 || (flags & ~1)) return -1;
     blocks = default_blocks(blocks);
     if (blocks <= 0) return -4;
-    stream_kernel<<<blocks, 256, 0, (hipStream_t)stream>>>((const u32x4*)buf, bytes / 16, sink);
+    hipStream_t s = (hipStream_t)stream;
+    if (flags & 1)
+        stream_kernel<true><<<blocks, 256, 0, s>>>((const u32x4*)buf, bytes / 16, sink);
+    else
+        stream_kernel<false><<<blocks, 256, 0, s>>>((const u32x4*)buf, bytes / 16, sink);
     return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
 int apex_hbm_probe_gather(const void* buf, const int32_t* chunk_ids, int64_t n_chunks, int blocks,
-                          uint32_t* sink, void* stream)
+                          int flags, uint32_t* sink, void* stream)
 {
-    if (!buf || !chunk_ids || !sink || n_chunks < 0 || blocks < 0) return -1;
+    if (!buf || !chunk_ids || !sink || n_chunks < 0 || blocks < 0 || (flags & ~0xf)) return -1;
+    const int unroll = (flags >> 1) & 7;
+    if (unroll != 1 && unroll != 2 && unroll != 4) return -1;
     if (n_chunks == 0) return 0;
     blocks = default_blocks(blocks);
     if (blocks <= 0) return -4;
-    gather_kernel<<<blocks, 256, 0, (hipStream_t)stream>>>((const u32x4*)buf, chunk_ids, n_chunks,
-                                                          sink);
+    hipStream_t s = (hipStream_t)stream;
+    const u32x4* p = (const u32x4*)buf;
+    const bool nt = flags & 1;
+    switch (unroll * 2 + (nt ? 1 : 0)) {
+        case 2: gather_kernel<1, false><<<blocks, 256, 0, s>>>(p, chunk_ids, n_chunks, sink); break;
+        case 3: gather_kernel<1, true><<<blocks, 256, 0, s>>>(p, chunk_ids, n_chunks, sink); break;
+        case 4: gather_kernel<2, false><<<blocks, 256, 0, s>>>(p, chunk_ids, n_chunks, sink); break;
+        case 5: gather_kernel<2, true><<<blocks, 256, 0, s>>>(p, chunk_ids, n_chunks, sink); break;
+        case 8: gather_kernel<4, false><<<blocks, 256, 0, s>>>(p, chunk_ids, n_chunks, sink); break;
+        default: gather_kernel<4, true><<<blocks, 256, 0, s>>>(p, chunk_ids, n_chunks, sink); break;
+    }
     return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 

@@ -44,8 +44,6 @@ struct AttnParams {
     const f16* q;          // [B][Hq][D]
     const f16* k;          // [NB][Hkv][BS][D]
     const f16* v;
-    const int32_t* bt;     // [B][stride]
-    const int32_t* lens;   // [B]
     f16* out;              // [B][Hq][D]
     float* lse;            // optional [B][Hq], natural log
     int32_t* counters;     // [B][Hkv] arrival counters, zero between calls
@@ -82,6 +80,19 @@ __device__ inline int uniform(int x)
     return __builtin_amdgcn_readfirstlane(x);
 }
 
+__device__ inline int64_t uniform64(int64_t x)
+{
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+template <typename T>
+__device__ inline T* uniform_ptr(T* p)
+{
+    return (T*)uniform64((int64_t)p);
+}
+
 // Device-scope coherent accesses (relaxed atomics at agent scope).  On gfx950
 // they carry the sc1 cache-coherence bit, so work groups on different XCDs
 // (each with its own L2) see each other's values without any cache flush.
@@ -109,103 +120,44 @@ __device__ inline unsigned pack_halves(unsigned a, unsigned b, unsigned sel)
     return __builtin_amdgcn_perm(b, a, sel);
 }
 
-// One 16-token block of one kv-head, as the MFMA operands want it.
-//   K: lane (t = lane % 16, q = lane / 16), word j = token t, dims [32j + 8q, +8)
-//   V: lane (c = lane % 16, q = lane / 16), word e = token 4q + e, dims [8c, 8c + 8)
-struct KVTile {
-    u32x4 k[4];
-    u32x4 v[4];
-};
+// One (block, kv-head) slab of K or V: 16 rows of 128 fp16 values.
+constexpr int kSlabBytes = kBlockSize * kHeadDim * 2;
+// Buffer-resource word 3 for raw (untyped) buffer access on gfx9-family GPUs.
+constexpr int kRawBufferWord3 = 0x00020000;
+// Cache policy of the K/V loads: non-temporal (bit 1) -- each row is read
+// exactly once per call, so it should not displace reusable lines.
+constexpr int kStreamingLoad = 2;
 
-__device__ inline void load_tile(KVTile& t, const f16* kb, const f16* vb, int lane)
+// Operand layouts of one slab (lane = 16 q + c, q = lane / 16, c = lane % 16):
+//   K: word i of lane (c, q) = token c, dims [32i + 8q, +8)   (A of S^T = K Q^T)
+//   V: word e of lane (c, q) = token 4q + e, dims [8c, 8c + 8)
+__device__ inline int k_lane_offset(int lane) { return (lane & 15) * 256 + (lane >> 4) * 16; }
+__device__ inline int v_lane_offset(int lane) { return (lane >> 4) * 1024 + (lane & 15) * 16; }
+
+// Loads a slab with buffer instructions: the slab base lives in scalar
+// registers (a fresh resource per block), the lane offset in a VGPR that
+// never changes.  The resource's extent bounds every access; an extent of 0
+// turns the four loads into no-ops that return zeros, which lets a pipeline
+// issue the same loads every step.
+__device__ inline void load_slab(u32x4 (&w)[4], const f16* slab, int bytes, int lane_off,
+                                 int stride)
 {
-    const int col = lane & 15, q = lane >> 4;
-    const f16* kp = kb + col * kHeadDim + 8 * q;
-    const f16* vp = vb + (4 * q) * kHeadDim + 8 * col;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        t.k[i] = *(const u32x4*)(kp + 32 * i);
-        t.v[i] = *(const u32x4*)(vp + i * kHeadDim);
-    }
-}
-
-// Online-softmax state of one wave.  Lane (h = lane % 16, q = lane / 16):
-// m = running max of head h (log2 units, equal on the four lanes of h),
-// l = running sum of the weights of the lane's tokens, acc[t][i] = running
-// P.V of head h at dim 32q + 8i + t.
-struct WaveState {
-    float m, l;
-    f32x4 acc[8];
-};
-
-// Scores, online softmax and P.V of one block.  tok0 = first token of the
-// block; tokens at or past L are masked (their V rows may hold anything).
-template <int G>
-__device__ inline void attend_tile(WaveState& st, KVTile& t, const f16x8 (&qop)[4], int tok0, int L,
-                                   float scale_log2, int lane)
-{
-    const int q = lane >> 4;
-    // S^T = K Q^T: lane (h, q) gets the scores of tokens 4q..4q+3 for head h
-    f32x4 s = {0.f, 0.f, 0.f, 0.f};
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc((void*)uniform_ptr(slab), (short)0, bytes, kRawBufferWord3);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-        s = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, t.k[i]), qop[i], s, 0, 0, 0);
-
-    float sv[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) sv[i] = s[i] * scale_log2;
-    if (tok0 + kBlockSize > L) {   // last, partial block of the pair
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            if (tok0 + 4 * q + i >= L) {
-                sv[i] = -INFINITY;
-                t.v[i] = u32x4{0u, 0u, 0u, 0u};
-            }
-        }
-    }
-
-    float bm = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-    bm = fmaxf(bm, wave_shfl_xor(bm, 16));
-    bm = fmaxf(bm, wave_shfl_xor(bm, 32));
-    const float mnew = fmaxf(st.m, bm);   // finite: the block holds a valid token
-    const float alpha = exp2_fast(st.m - mnew);
-    f32x4 pw;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) pw[i] = exp2_fast(sv[i] - mnew);
-    const f16x4 ph = __builtin_convertvector(pw, f16x4);
-    // the normaliser uses the same fp16-rounded weights as the numerator
-    const float psum = ((float)ph[0] + (float)ph[1]) + ((float)ph[2] + (float)ph[3]);
-    st.l = st.l * alpha + psum;
-    if (alpha != 1.f) {
-#pragma unroll
-        for (int tt = 0; tt < 8; ++tt) st.acc[tt] *= alpha;
-    }
-    st.m = mnew;
-
-    // O^T += V^T P^T, eight 16-dim tiles; tile tt row c is dim 8c + tt
-#pragma unroll
-    for (int tt = 0; tt < 8; ++tt) {
-        const int w = tt >> 1;
-        const unsigned sel = (tt & 1) ? kHiHalves : kLoHalves;
-        unsigned a0, a1;
-        switch (w) {
-            case 0: a0 = pack_halves(t.v[0].x, t.v[1].x, sel); a1 = pack_halves(t.v[2].x, t.v[3].x, sel); break;
-            case 1: a0 = pack_halves(t.v[0].y, t.v[1].y, sel); a1 = pack_halves(t.v[2].y, t.v[3].y, sel); break;
-            case 2: a0 = pack_halves(t.v[0].z, t.v[1].z, sel); a1 = pack_halves(t.v[2].z, t.v[3].z, sel); break;
-            default: a0 = pack_halves(t.v[0].w, t.v[1].w, sel); a1 = pack_halves(t.v[2].w, t.v[3].w, sel); break;
-        }
-        typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
-        const u32x2 a = {a0, a1};
-        st.acc[tt] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, a), ph, st.acc[tt], 0, 0, 0);
-    }
+        w[i] = __builtin_amdgcn_raw_buffer_load_b128(r, lane_off + stride * i, 0, kStreamingLoad);
 }
 
 // Per-wave attention over blocks lo + wave, lo + wave + 4, ... < hi of pair
-// (b, g).  On return the wave's state is in s_acc/s_m/s_l.
+// (b, g).  Lane (h = lane % 16, q = lane / 16) keeps m (running max of head
+// h, log2 units, equal on the four lanes of h), l (sum of the weights of its
+// tokens) and acc[t][i] (running P.V of head h at dim 32q + 8i + t).  On
+// return the wave's state is in s_acc/s_m/s_l.
 template <int G>
-__device__ inline void wave_attend(const AttnParams& p, const int32_t* bt_row, int b, int g, int L,
-                                   int lo, int hi, int wave, int lane, float (*s_acc)[G][kHeadDim],
-                                   float (*s_m)[G], float (*s_l)[G])
+__device__ inline void wave_attend(const AttnParams& p, const int32_t* __restrict__ bt_row, int b,
+                                   int g, int L, int lo, int hi, int wave, int lane,
+                                   float (*s_acc)[G][kHeadDim], float (*s_m)[G], float (*s_l)[G])
 {
     constexpr int D = kHeadDim;
     constexpr int BS = kBlockSize;
@@ -224,50 +176,113 @@ __device__ inline void wave_attend(const AttnParams& p, const int32_t* bt_row, i
         for (int i = 0; i < 4; ++i) qop[i] = f16x8{0, 0, 0, 0, 0, 0, 0, 0};
     }
 
-    WaveState st;
-    st.m = -INFINITY;
-    st.l = 0.f;
+    float m = -INFINITY, l = 0.f;
+    f32x4 acc[8];
 #pragma unroll
-    for (int tt = 0; tt < 8; ++tt) st.acc[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < 8; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const size_t head_off = (size_t)g * (BS * D);
-    const size_t blk_elems = (size_t)p.Hkv * BS * D;
-    KVTile ta, tb;
-    int j = lo + wave;
-    if (j < hi) {
-        const size_t base = (size_t)uniform(bt_row[j]) * blk_elems + head_off;
-        load_tile(ta, p.k + base, p.v + base, lane);
-    }
-    while (j < hi) {
-        int jn = j + kWaves;
-        if (jn < hi) {
-            const size_t base = (size_t)uniform(bt_row[jn]) * blk_elems + head_off;
-            load_tile(tb, p.k + base, p.v + base, lane);
+    // This wave's blocks are first + kWaves * k, k = 0 .. n - 1.  Slab
+    // addresses are formed in scalar registers only, block ids arrive through
+    // the scalar path (the table is a read-only restrict argument) two steps
+    // ahead, and every step issues the next block's eight loads.
+    const int first = uniform(lo + wave);
+    const int n = first < hi ? (hi - first + kWaves - 1) / kWaves : 0;
+    const int32_t* __restrict__ bt_w = bt_row + first;
+    const size_t head_off = (size_t)uniform(g) * (BS * D);
+    const f16* kpair = uniform_ptr(p.k + head_off);
+    const f16* vpair = uniform_ptr(p.v + head_off);
+    const uint32_t step = (uint32_t)((size_t)p.Hkv * BS * D);
+    const int koff = k_lane_offset(lane);
+    const int voff = v_lane_offset(lane);
+
+    u32x4 kt[4], vt[4];
+    const int id0 = n > 0 ? bt_w[0] : 0;
+    int id_nxt = n > 1 ? bt_w[kWaves] : 0;
+    load_slab(kt, kpair + (uint64_t)(uint32_t)id0 * step, n > 0 ? kSlabBytes : 0, koff, 64);
+    load_slab(vt, vpair + (uint64_t)(uint32_t)id0 * step, n > 0 ? kSlabBytes : 0, voff, 256);
+
+    for (int k = 0; k < n; ++k) {
+        const int id_after = k + 2 < n ? bt_w[kWaves * (k + 2)] : 0;
+        const int nbytes = k + 1 < n ? kSlabBytes : 0;
+        const int tok0 = (first + kWaves * k) * BS;
+
+        // S^T = K Q^T: lane (h, q) gets the scores of tokens 4q..4q+3 of head h
+        f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            s = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, kt[i]), qop[i], s, 0, 0, 0);
+        // K is consumed: refill it with the next block
+        load_slab(kt, kpair + (uint64_t)(uint32_t)id_nxt * step, nbytes, koff, 64);
+
+        float sv[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sv[i] = s[i] * p.scale_log2;
+        const bool tail = tok0 + BS > L;   // the pair's last, partial block
+        if (tail) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (tok0 + 4 * q + i >= L) sv[i] = -INFINITY;
         }
-        attend_tile<G>(st, ta, qop, j * BS, L, p.scale_log2, lane);
-        j = jn;
-        if (j >= hi) break;
-        jn = j + kWaves;
-        if (jn < hi) {
-            const size_t base = (size_t)uniform(bt_row[jn]) * blk_elems + head_off;
-            load_tile(ta, p.k + base, p.v + base, lane);
+        float bm = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+        bm = fmaxf(bm, wave_shfl_xor(bm, 16));
+        bm = fmaxf(bm, wave_shfl_xor(bm, 32));
+        const float mnew = fmaxf(m, bm);   // finite: the block holds a valid token
+        const float alpha = exp2_fast(m - mnew);
+        f32x4 pw;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pw[i] = exp2_fast(sv[i] - mnew);
+        const f16x4 ph = __builtin_convertvector(pw, f16x4);
+        // the normaliser uses the same fp16-rounded weights as the numerator
+        l = l * alpha + (((float)ph[0] + (float)ph[1]) + ((float)ph[2] + (float)ph[3]));
+        m = mnew;
+
+        // V^T operands in registers: tile t row c is dim 8c + t, its k index
+        // is token 4q + e; rows of masked tokens are zeroed (they may hold NaN)
+        unsigned a[8][2];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const unsigned sel = (t & 1) ? kHiHalves : kLoHalves;
+            const int w = t >> 1;
+            a[t][0] = pack_halves(vt[0][w], vt[1][w], sel);
+            a[t][1] = pack_halves(vt[2][w], vt[3][w], sel);
         }
-        attend_tile<G>(st, tb, qop, j * BS, L, p.scale_log2, lane);
-        j = jn;
+        // V is consumed: refill it with the next block
+        load_slab(vt, vpair + (uint64_t)(uint32_t)id_nxt * step, nbytes, voff, 256);
+        if (tail) {
+            const bool ok0 = tok0 + 4 * q + 0 < L, ok1 = tok0 + 4 * q + 1 < L;
+            const bool ok2 = tok0 + 4 * q + 2 < L, ok3 = tok0 + 4 * q + 3 < L;
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                a[t][0] = (ok0 ? a[t][0] & 0x0000ffffu : 0u) | (ok1 ? a[t][0] & 0xffff0000u : 0u);
+                a[t][1] = (ok2 ? a[t][1] & 0x0000ffffu : 0u) | (ok3 ? a[t][1] & 0xffff0000u : 0u);
+            }
+        }
+        if (alpha != 1.f) {
+#pragma unroll
+            for (int t = 0; t < 8; ++t) acc[t] *= alpha;
+        }
+        // O^T += V^T P^T, eight 16-dim tiles
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+            const u32x2 av = {a[t][0], a[t][1]};
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, av), ph, acc[t], 0, 0, 0);
+        }
+        id_nxt = id_after;
     }
 
     // the wave's state for head h: l summed over the four token groups
-    float lw = st.l + wave_shfl_xor(st.l, 16);
+    float lw = l + wave_shfl_xor(l, 16);
     lw += wave_shfl_xor(lw, 32);
     if (col < G) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             float* dst = &s_acc[wave][col][32 * q + 8 * i];
-            *(f32x4*)dst = f32x4{st.acc[0][i], st.acc[1][i], st.acc[2][i], st.acc[3][i]};
-            *(f32x4*)(dst + 4) = f32x4{st.acc[4][i], st.acc[5][i], st.acc[6][i], st.acc[7][i]};
+            *(f32x4*)dst = f32x4{acc[0][i], acc[1][i], acc[2][i], acc[3][i]};
+            *(f32x4*)(dst + 4) = f32x4{acc[4][i], acc[5][i], acc[6][i], acc[7][i]};
         }
         if (q == 0) {
-            s_m[wave][col] = st.m;
+            s_m[wave][col] = m;
             s_l[wave][col] = lw;
         }
     }
@@ -284,7 +299,9 @@ __device__ inline void write_row(const AttnParams& p, int b, int head, int dim, 
 }
 
 template <int G>
-__global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2))) void attn_kernel(AttnParams p)
+__global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(3))) void attn_kernel(AttnParams p,
+                                                        const int32_t* __restrict__ bt,
+                                                        const int32_t* __restrict__ lens)
 {
     constexpr int D = kHeadDim;
     __shared__ float s_acc[kWaves][G][D];
@@ -304,7 +321,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
 
     // rows of empty requests are zeros (and lse = -inf)
     for (int b = (int)w; b < B; b += (int)gridDim.x) {
-        if (p.lens[b] <= 0) {
+        if (lens[b] <= 0) {
             for (int i = tid; i < p.Hq * D; i += kAttnThreads) write_row(p, b, i / D, i % D, 0.f, 0.f, 0.f);
         }
     }
@@ -315,7 +332,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     const int r1 = min(B, r0 + seg);
     int tsum = 0, tmax = 0;
     for (int b = r0; b < r1; ++b) {
-        const int nb = (int)blocks_of(p.lens[b], kBlockSize);
+        const int nb = (int)blocks_of(lens[b], kBlockSize);
         tsum += nb;
         tmax = max(tmax, nb);
     }
@@ -329,8 +346,8 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         s_scan[tid] += v;
         __syncthreads();
     }
-    const int64_t units = (int64_t)s_scan[kAttnThreads - 1] * p.Hkv;
-    const int64_t stride = p.bt_stride > 0 ? p.bt_stride : (int64_t)s_maxb;
+    const int64_t units = (int64_t)uniform(s_scan[kAttnThreads - 1]) * p.Hkv;
+    const int64_t stride = p.bt_stride > 0 ? p.bt_stride : (int64_t)uniform(s_maxb);
     const int64_t W = active_workers(units, (int64_t)gridDim.x, p.min_units);
     if (w >= W || units == 0) return;
     const int64_t u0 = worker_start(w, units, W);
@@ -343,7 +360,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         if (excl * p.Hkv <= u0 && u0 < (int64_t)s_scan[tid] * p.Hkv) {
             int64_t pre = excl;
             for (int b = r0; b < r1; ++b) {
-                const int64_t nb = blocks_of(p.lens[b], kBlockSize);
+                const int64_t nb = blocks_of(lens[b], kBlockSize);
                 if (u0 < (pre + nb) * p.Hkv) {
                     s_loc_b = b;
                     s_loc_pre = pre;
@@ -356,19 +373,19 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     __syncthreads();
 
     int b = uniform(s_loc_b);
-    int64_t pre = s_loc_pre;
-    int L = uniform(p.lens[b]);
+    int64_t pre = uniform64(s_loc_pre);
+    int L = uniform(lens[b]);
     int nb = (int)blocks_of(L, kBlockSize);
     int64_t off = u0 - pre * p.Hkv;
-    int g = (int)(off / nb);
-    int blk = (int)(off % nb);
+    int g = uniform((int)(off / nb));
+    int blk = uniform((int)(off % nb));
     int64_t u = u0;
 
     // 2. segments
     while (true) {
         const int take = (int)min((int64_t)(nb - blk), u1 - u);
         const int lo = blk, hi = blk + take;
-        const int32_t* bt_row = p.bt + (size_t)b * (size_t)stride;
+        const int32_t* bt_row = bt + (size_t)uniform(b) * (size_t)stride;
         wave_attend<G>(p, bt_row, b, g, L, lo, hi, wave, lane, s_acc, s_m, s_l);
         __syncthreads();
 
@@ -447,9 +464,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
                 pre += nb;
                 do {
                     ++b;
-                } while (b < B && p.lens[b] <= 0);
+                } while (b < B && lens[b] <= 0);
                 if (b >= B) break;   // unreachable: units remain after the current pair
-                L = uniform(p.lens[b]);
+                L = uniform(lens[b]);
                 nb = (int)blocks_of(L, kBlockSize);
             }
         }

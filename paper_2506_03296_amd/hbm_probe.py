@@ -19,9 +19,10 @@ def load_library():
         lib = ctypes.CDLL(LIB_PATH)
         vp = ctypes.c_void_p
         lib.apex_hbm_probe_stream.restype = ctypes.c_int
-        lib.apex_hbm_probe_stream.argtypes = [vp, ctypes.c_size_t, ctypes.c_int, vp, vp]
+        lib.apex_hbm_probe_stream.argtypes = [vp, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, vp, vp]
         lib.apex_hbm_probe_gather.restype = ctypes.c_int
-        lib.apex_hbm_probe_gather.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int, vp, vp]
+        lib.apex_hbm_probe_gather.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                                              vp, vp]
         _LIB = lib
     return _LIB
 
@@ -40,7 +41,8 @@ def _time(torch, fn, reps):
 
 
 def measure(nbytes=4 << 30, reps=10, blocks_list=(0,), seed=0):
-    """Returns {"stream": {blocks: GB/s}, "gather4k": {blocks: GB/s}}."""
+    """Returns GB/s per (pattern, flags, blocks): "stream" (flags = nt) and
+    "gather4k" (flags = nt | chunks-in-flight << 1)."""
     import torch
     lib = load_library()
     buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
@@ -53,13 +55,18 @@ def measure(nbytes=4 << 30, reps=10, blocks_list=(0,), seed=0):
     stream = torch.cuda.current_stream().cuda_stream
     res = {"bytes": nbytes, "stream": {}, "gather4k": {}}
     for blocks in blocks_list:
-        def f1():
-            rc = lib.apex_hbm_probe_stream(buf.data_ptr(), nbytes, blocks, sink.data_ptr(), stream)
-            assert rc == 0
-        def f2():
-            rc = lib.apex_hbm_probe_gather(buf.data_ptr(), ids.data_ptr(), n_chunks, blocks,
-                                           sink.data_ptr(), stream)
-            assert rc == 0
-        res["stream"][blocks] = round(nbytes / _time(torch, f1, reps) / 1e9, 1)
-        res["gather4k"][blocks] = round(nbytes / _time(torch, f2, reps) / 1e9, 1)
+        for nt in (0, 1):
+            def f1():
+                rc = lib.apex_hbm_probe_stream(buf.data_ptr(), nbytes, blocks, nt, sink.data_ptr(),
+                                               stream)
+                assert rc == 0
+            res["stream"][f"nt{nt}_wg{blocks}"] = round(nbytes / _time(torch, f1, reps) / 1e9, 1)
+            for unroll in (1, 2, 4):
+                flags = nt | (unroll << 1)
+                def f2():
+                    rc = lib.apex_hbm_probe_gather(buf.data_ptr(), ids.data_ptr(), n_chunks, blocks,
+                                                   flags, sink.data_ptr(), stream)
+                    assert rc == 0
+                res["gather4k"][f"nt{nt}_u{unroll}_wg{blocks}"] = round(
+                    nbytes / _time(torch, f2, reps) / 1e9, 1)
     return res
