@@ -2,8 +2,8 @@
 //
 // One call = one launch of attn_kernel<G> on a persistent grid of W work
 // groups (4 waves each).  Every work group
-//   1. reads context_lens and derives the partition of plan_policy.h on its
-//      own (block sums, a prefix scan, the longest request for the tight
+//   1. reads context_lens once and derives the partition of plan_policy.h on
+//      its own (block sums, a prefix scan, the longest request for the tight
 //      block-table stride), so no planner kernel runs before it;
 //   2. walks its contiguous range of (request b, kv-head g, block) units
 //      segment by segment.  In a segment the four waves take the blocks of
@@ -17,7 +17,8 @@
 //   3. merges the waves' states in LDS and either writes the fp16 output rows
 //      (the segment is the whole pair) or stores an fp32 partial
 //      (accumulator, max, sum) and bumps the pair's arrival counter; the last
-//      work group to arrive combines the pair's partials and writes the rows.
+//      work group to arrive combines the pair's partials and writes the rows;
+//   4. writes the zero rows of requests with no context (their share of them).
 //
 // The attention is the standard softmax attention that APEX runs for its
 // GPU-resident decode requests over their paged KV (Sec. 3.1, Sec. 3.3,
@@ -39,6 +40,7 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kAttnThreads = 256;
 constexpr int kWaves = kAttnThreads / 64;
+constexpr int kCachedLens = 2048;   // context_lens kept in LDS up to this batch size
 
 struct AttnParams {
     const f16* q;          // [B][Hq][D]
@@ -307,8 +309,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(3)
     __shared__ float s_acc[kWaves][G][D];
     __shared__ float s_m[kWaves][G];
     __shared__ float s_l[kWaves][G];
-    __shared__ int s_scan[kAttnThreads];
-    __shared__ int s_maxb;
+    __shared__ int s_lens[kCachedLens];
+    __shared__ int s_wsum[kWaves];
+    __shared__ int s_wmax[kWaves];
     __shared__ int s_loc_b;
     __shared__ int64_t s_loc_pre;
     __shared__ int s_last;
@@ -318,49 +321,57 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(3)
     const int wave = tid >> 6;
     const int64_t w = blockIdx.x;
     const int B = p.B;
+    const bool cached = B <= kCachedLens;
 
-    // rows of empty requests are zeros (and lse = -inf)
-    for (int b = (int)w; b < B; b += (int)gridDim.x) {
-        if (lens[b] <= 0) {
-            for (int i = tid; i < p.Hq * D; i += kAttnThreads) write_row(p, b, i / D, i % D, 0.f, 0.f, 0.f);
-        }
-    }
-
-    // 1. partition: block sums per thread segment, scan, longest request
+    // 1. partition.  context_lens is read from memory once: each thread sums
+    // the blocks of a contiguous run of requests (and keeps the lengths in
+    // LDS when they fit); wave-level scans plus one barrier give the prefix
+    // sums, the total and the longest request.
     const int seg = (B + kAttnThreads - 1) / kAttnThreads;
     const int r0 = min(B, tid * seg);
     const int r1 = min(B, r0 + seg);
     int tsum = 0, tmax = 0;
     for (int b = r0; b < r1; ++b) {
-        const int nb = (int)blocks_of(lens[b], kBlockSize);
+        const int L = lens[b];
+        if (cached) s_lens[b] = L;
+        const int nb = (int)blocks_of(L, kBlockSize);
         tsum += nb;
         tmax = max(tmax, nb);
     }
-    if (tid == 0) s_maxb = 0;
-    s_scan[tid] = tsum;
-    __syncthreads();
-    atomicMax(&s_maxb, tmax);
-    for (int off = 1; off < kAttnThreads; off <<= 1) {
-        const int v = tid >= off ? s_scan[tid - off] : 0;
-        __syncthreads();
-        s_scan[tid] += v;
-        __syncthreads();
+    int incl = tsum;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int y = __shfl_up(incl, d, 64);
+        if (lane >= d) incl += y;
     }
-    const int64_t units = (int64_t)uniform(s_scan[kAttnThreads - 1]) * p.Hkv;
-    const int64_t stride = p.bt_stride > 0 ? p.bt_stride : (int64_t)uniform(s_maxb);
-    const int64_t W = active_workers(units, (int64_t)gridDim.x, p.min_units);
-    if (w >= W || units == 0) return;
-    const int64_t u0 = worker_start(w, units, W);
-    const int64_t u1 = worker_start(w + 1, units, W);
-    if (u0 >= u1) return;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) tmax = max(tmax, __shfl_xor(tmax, d, 64));
+    if (lane == 63) s_wsum[wave] = incl;
+    if (lane == 0) s_wmax[wave] = tmax;
+    __syncthreads();
+    int total = 0, maxb = 0;
+#pragma unroll
+    for (int v = 0; v < kWaves; ++v) {
+        if (v < wave) incl += s_wsum[v];
+        total += s_wsum[v];
+        maxb = max(maxb, s_wmax[v]);
+    }
+    auto len_of = [&](int b) -> int { return cached ? s_lens[b] : lens[b]; };
 
+    const int64_t units = (int64_t)uniform(total) * p.Hkv;
+    const int64_t stride = p.bt_stride > 0 ? p.bt_stride : (int64_t)uniform(maxb);
+    const int64_t W = active_workers(units, (int64_t)gridDim.x, p.min_units);
+    const int64_t u0 = units > 0 && w < W ? worker_start(w, units, W) : 0;
+    const int64_t u1 = units > 0 && w < W ? worker_start(w + 1, units, W) : 0;
+
+    if (u0 < u1) {
     // locate the pair holding unit u0
     {
-        const int64_t excl = s_scan[tid] - tsum;
-        if (excl * p.Hkv <= u0 && u0 < (int64_t)s_scan[tid] * p.Hkv) {
+        const int64_t excl = incl - tsum;
+        if (excl * p.Hkv <= u0 && u0 < (int64_t)incl * p.Hkv) {
             int64_t pre = excl;
             for (int b = r0; b < r1; ++b) {
-                const int64_t nb = blocks_of(lens[b], kBlockSize);
+                const int64_t nb = blocks_of(len_of(b), kBlockSize);
                 if (u0 < (pre + nb) * p.Hkv) {
                     s_loc_b = b;
                     s_loc_pre = pre;
@@ -374,7 +385,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(3)
 
     int b = uniform(s_loc_b);
     int64_t pre = uniform64(s_loc_pre);
-    int L = uniform(lens[b]);
+    int L = uniform(len_of(b));
     int nb = (int)blocks_of(L, kBlockSize);
     int64_t off = u0 - pre * p.Hkv;
     int g = uniform((int)(off / nb));
@@ -464,11 +475,19 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(3)
                 pre += nb;
                 do {
                     ++b;
-                } while (b < B && lens[b] <= 0);
+                } while (b < B && len_of(b) <= 0);
                 if (b >= B) break;   // unreachable: units remain after the current pair
-                L = uniform(lens[b]);
+                L = uniform(len_of(b));
                 nb = (int)blocks_of(L, kBlockSize);
             }
+        }
+    }
+    }
+
+    // rows of empty requests are zeros (and lse = -inf)
+    for (int b = (int)w; b < B; b += (int)gridDim.x) {
+        if (len_of(b) <= 0) {
+            for (int i = tid; i < p.Hq * D; i += kAttnThreads) write_row(p, b, i / D, i % D, 0.f, 0.f, 0.f);
         }
     }
 }
