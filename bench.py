@@ -113,6 +113,8 @@ def main():
                     help="only run a plain device copy of MIB MiB (for counter scaling)")
     ap.add_argument("--hbm-probe", action="store_true",
                     help="only measure achievable HBM read bandwidth (stream and 4 KiB gather)")
+    ap.add_argument("--probe-mib", type=int, default=4096,
+                    help="buffer size of --hbm-probe in MiB")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -144,7 +146,7 @@ def main():
         from paper_2506_03296_amd import hbm_probe
         props = torch.cuda.get_device_properties(0)
         cus = props.multi_processor_count
-        res = hbm_probe.measure(blocks_list=(cus * 2, cus * 4, cus * 8))
+        res = hbm_probe.measure(nbytes=args.probe_mib << 20, blocks_list=(cus * 2, cus * 4, cus * 8))
         res["device"] = props.name
         res["cus"] = cus
         print(json.dumps(res), flush=True)

@@ -41,6 +41,7 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kAttnThreads = 256;
 constexpr int kWaves = kAttnThreads / 64;
 constexpr int kCachedLens = 2048;   // context_lens kept in LDS up to this batch size
+constexpr int kCombineChunk = 8;    // partials loaded at once by the combining work group
 
 struct AttnParams {
     const f16* q;          // [B][Hq][D]
@@ -183,10 +184,13 @@ __device__ inline void wave_attend(const AttnParams& p, const int32_t* __restric
 #pragma unroll
     for (int t = 0; t < 8; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // This wave's blocks are first + kWaves * k, k = 0 .. n - 1.  Slab
-    // addresses are formed in scalar registers only, block ids arrive through
-    // the scalar path (the table is a read-only restrict argument) two steps
-    // ahead, and every step issues the next block's eight loads.
+    // This wave's blocks are first + kWaves * k, k = 0 .. n - 1.  Two K/V
+    // tiles alternate and each step refills the tile it consumed with the
+    // block two steps ahead, so two blocks (16 KiB) stay in flight per wave.
+    // Slab addresses are formed in scalar registers only, block ids arrive
+    // through the scalar path (the table is a read-only restrict argument)
+    // ahead of use, and every step issues eight loads (zero-extent past the
+    // end) so the compiler can wait for exactly the oldest slab.
     const int first = uniform(lo + wave);
     const int n = first < hi ? (hi - first + kWaves - 1) / kWaves : 0;
     const int32_t* __restrict__ bt_w = bt_row + first;
@@ -196,16 +200,12 @@ __device__ inline void wave_attend(const AttnParams& p, const int32_t* __restric
     const uint32_t step = (uint32_t)((size_t)p.Hkv * BS * D);
     const int koff = k_lane_offset(lane);
     const int voff = v_lane_offset(lane);
+    auto id_of = [&](int k) -> int { return k < n ? bt_w[kWaves * k] : 0; };
+    auto bytes_of = [&](int k) -> int { return k < n ? kSlabBytes : 0; };
 
-    u32x4 kt[4], vt[4];
-    const int id0 = n > 0 ? bt_w[0] : 0;
-    int id_nxt = n > 1 ? bt_w[kWaves] : 0;
-    load_slab(kt, kpair + (uint64_t)(uint32_t)id0 * step, n > 0 ? kSlabBytes : 0, koff, 64);
-    load_slab(vt, vpair + (uint64_t)(uint32_t)id0 * step, n > 0 ? kSlabBytes : 0, voff, 256);
-
-    for (int k = 0; k < n; ++k) {
-        const int id_after = k + 2 < n ? bt_w[kWaves * (k + 2)] : 0;
-        const int nbytes = k + 1 < n ? kSlabBytes : 0;
+    // One block: consume (kt, vt), refill them with block k + 2 (id2).
+    auto block_step = [&](u32x4 (&kt)[4], u32x4 (&vt)[4], int k, int id2) {
+        const int nbytes = bytes_of(k + 2);
         const int tok0 = (first + kWaves * k) * BS;
 
         // S^T = K Q^T: lane (h, q) gets the scores of tokens 4q..4q+3 of head h
@@ -213,8 +213,8 @@ __device__ inline void wave_attend(const AttnParams& p, const int32_t* __restric
 #pragma unroll
         for (int i = 0; i < 4; ++i)
             s = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, kt[i]), qop[i], s, 0, 0, 0);
-        // K is consumed: refill it with the next block
-        load_slab(kt, kpair + (uint64_t)(uint32_t)id_nxt * step, nbytes, koff, 64);
+        // K is consumed: refill it
+        load_slab(kt, kpair + (uint64_t)(uint32_t)id2 * step, nbytes, koff, 64);
 
         float sv[4];
 #pragma unroll
@@ -248,8 +248,8 @@ __device__ inline void wave_attend(const AttnParams& p, const int32_t* __restric
             a[t][0] = pack_halves(vt[0][w], vt[1][w], sel);
             a[t][1] = pack_halves(vt[2][w], vt[3][w], sel);
         }
-        // V is consumed: refill it with the next block
-        load_slab(vt, vpair + (uint64_t)(uint32_t)id_nxt * step, nbytes, voff, 256);
+        // V is consumed: refill it
+        load_slab(vt, vpair + (uint64_t)(uint32_t)id2 * step, nbytes, voff, 256);
         if (tail) {
             const bool ok0 = tok0 + 4 * q + 0 < L, ok1 = tok0 + 4 * q + 1 < L;
             const bool ok2 = tok0 + 4 * q + 2 < L, ok3 = tok0 + 4 * q + 3 < L;
@@ -270,7 +270,25 @@ __device__ inline void wave_attend(const AttnParams& p, const int32_t* __restric
             const u32x2 av = {a[t][0], a[t][1]};
             acc[t] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, av), ph, acc[t], 0, 0, 0);
         }
-        id_nxt = id_after;
+    };
+
+    u32x4 kt0[4], vt0[4], kt1[4], vt1[4];
+    {
+        const int id0 = id_of(0), id1 = id_of(1);
+        load_slab(kt0, kpair + (uint64_t)(uint32_t)id0 * step, bytes_of(0), koff, 64);
+        load_slab(vt0, vpair + (uint64_t)(uint32_t)id0 * step, bytes_of(0), voff, 256);
+        load_slab(kt1, kpair + (uint64_t)(uint32_t)id1 * step, bytes_of(1), koff, 64);
+        load_slab(vt1, vpair + (uint64_t)(uint32_t)id1 * step, bytes_of(1), voff, 256);
+    }
+    int ida = id_of(2), idb = id_of(3);   // ids of the blocks two steps ahead
+    for (int k = 0; k < n; k += 2) {
+        const int ida_next = id_of(k + 4);
+        block_step(kt0, vt0, k, ida);
+        ida = ida_next;
+        if (k + 1 >= n) break;
+        const int idb_next = id_of(k + 5);
+        block_step(kt1, vt1, k + 1, idb);
+        idb = idb_next;
     }
 
     // the wave's state for head h: l summed over the four token groups
@@ -301,7 +319,7 @@ __device__ inline void write_row(const AttnParams& p, int b, int head, int dim, 
 }
 
 template <int G>
-__global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(3))) void attn_kernel(AttnParams p,
+__global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2))) void attn_kernel(AttnParams p,
                                                         const int32_t* __restrict__ bt,
                                                         const int32_t* __restrict__ lens)
 {
@@ -444,20 +462,41 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(3)
             }
             __syncthreads();
             if (s_last) {
+                // combine the pair's partials: each thread issues the loads of
+                // kCombineChunk contributors at once, then folds them in with
+                // an online rescale (running max M, numerator, denominator)
+                const int nc = (int)(wl - wf + 1);
                 for (int idx = tid; idx < G * D; idx += kAttnThreads) {
                     const int h = idx / D, dim = idx % D;
-                    float M = -INFINITY;
-                    for (int64_t q = wf; q <= wl; ++q) {
-                        const int64_t sq = partial_slot(q, p0, units, W);
-                        M = fmaxf(M, load_coherent(&p.pml[((size_t)sq * G + h) * 2]));
-                    }
-                    const float Ms = M == -INFINITY ? 0.f : M;
-                    float num = 0.f, den = 0.f;
-                    for (int64_t q = wf; q <= wl; ++q) {
-                        const int64_t sq = partial_slot(q, p0, units, W);
-                        const float f = exp2_fast(load_coherent(&p.pml[((size_t)sq * G + h) * 2]) - Ms);
-                        num = fmaf(f, load_coherent(&p.pacc[((size_t)sq * G + h) * D + dim]), num);
-                        den = fmaf(f, load_coherent(&p.pml[((size_t)sq * G + h) * 2 + 1]), den);
+                    float M = -INFINITY, num = 0.f, den = 0.f;
+                    for (int c0 = 0; c0 < nc; c0 += kCombineChunk) {
+                        float cm[kCombineChunk], cl[kCombineChunk], ca[kCombineChunk];
+#pragma unroll
+                        for (int j = 0; j < kCombineChunk; ++j) {
+                            cm[j] = -INFINITY;
+                            cl[j] = 0.f;
+                            ca[j] = 0.f;
+                            if (c0 + j < nc) {
+                                const int64_t sq = partial_slot(wf + c0 + j, p0, units, W);
+                                cm[j] = load_coherent(&p.pml[((size_t)sq * G + h) * 2]);
+                                cl[j] = load_coherent(&p.pml[((size_t)sq * G + h) * 2 + 1]);
+                                ca[j] = load_coherent(&p.pacc[((size_t)sq * G + h) * D + dim]);
+                            }
+                        }
+                        float Mn = M;
+#pragma unroll
+                        for (int j = 0; j < kCombineChunk; ++j) Mn = fmaxf(Mn, cm[j]);
+                        const float Ms = Mn == -INFINITY ? 0.f : Mn;
+                        const float r = exp2_fast(M - Ms);
+                        num *= r;
+                        den *= r;
+#pragma unroll
+                        for (int j = 0; j < kCombineChunk; ++j) {
+                            const float f = exp2_fast(cm[j] - Ms);
+                            num = fmaf(f, ca[j], num);
+                            den = fmaf(f, cl[j], den);
+                        }
+                        M = Mn;
                     }
                     write_row(p, b, g * G + h, dim, M, num, den);
                 }
