@@ -291,3 +291,46 @@ def fp16_digest(*arrays):
     for a in arrays:
         h.update(np.ascontiguousarray(a).tobytes())
     return h.hexdigest()
+
+
+def append_slots(layout, block_size=BLOCK_SIZE):
+    """Cache slot of each request's newest token (position L_b - 1), as an
+    engine assigns it before the step: block_table[b][(L-1) // bs] * bs +
+    (L-1) % bs; -1 (padding) for L_b <= 0.  int64 [B]."""
+    slots = np.full(len(layout.lens), -1, dtype=np.int64)
+    for b, L in enumerate(layout.lens):
+        L = int(L)
+        if L > 0:
+            slots[b] = int(layout.block_table[b, (L - 1) // block_size]) * block_size + (L - 1) % block_size
+    return slots
+
+
+@dataclass
+class AppendCase:
+    """Inputs of one KV append: caches, new rows and their slots (host)."""
+    k_cache: np.ndarray       # float16 [NB][Hkv][bs][d]
+    v_cache: np.ndarray
+    k_new: np.ndarray         # float16 [T][Hkv][d]
+    v_new: np.ndarray
+    slot_mapping: np.ndarray  # int64 [T]
+
+
+def make_append_case(T, num_blocks, Hkv, d=D_HEAD, block_size=BLOCK_SIZE, seed=0,
+                     padding=0, out_of_range=0):
+    """T new tokens with distinct random slots in a pool of ``num_blocks``
+    blocks; ``padding`` of them get slot -1 and ``out_of_range`` of them a
+    slot at or past the pool's end."""
+    rng = np.random.default_rng(seed)
+    cap = num_blocks * block_size
+    if T - padding - out_of_range > cap:
+        raise ValueError("more tokens than slots")
+    slots = rng.choice(cap, size=T - padding - out_of_range, replace=False).astype(np.int64)
+    extra = np.concatenate([np.full(padding, -1, dtype=np.int64),
+                            cap + rng.integers(0, 4 * block_size, size=out_of_range)])
+    slots = np.concatenate([slots, extra])
+    rng.shuffle(slots)
+    k = rng.standard_normal((num_blocks, Hkv, block_size, d)).astype(np.float16)
+    v = rng.standard_normal((num_blocks, Hkv, block_size, d)).astype(np.float16)
+    kn = rng.standard_normal((T, Hkv, d)).astype(np.float16)
+    vn = rng.standard_normal((T, Hkv, d)).astype(np.float16)
+    return AppendCase(k, v, kn, vn, slots)
