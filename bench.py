@@ -16,6 +16,11 @@ JSON line:
              when it was taken on the current kernel source, else null
   cpu_baseline  the fp64 CPU oracle on the host cores over a bounded sample of
              the same workload (the first requests), in the same unit
+  kv_append  the paged KV append that precedes each step (apex_kv_append),
+             timed alone with events around its kernel: the step's own append
+             (one token per request at position L_b - 1 of the workload's
+             cache) and a prompt-sized bulk append (65536 tokens) against the
+             HBM peak; bytes = new K/V rows read + cache rows written + slots
 
 The default workload is the Llama-3.1-8B GQA long-output decode batch (B=32,
 32 q-heads over 8 kv-heads, d=128, block_size 16, context lengths lognormal
@@ -36,8 +41,10 @@ if ROOT not in sys.path:
 METRIC = "decode-attn µs/layer-step + achieved HBM GB/s (% peak), Llama-3.1-8B GQA"
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
+# the files that define the attention kernel and its work partition: counter
+# summaries stay valid while these are unchanged
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2506_03296_amd", "csrc", f)
-                  for f in ("kernels.h", "plan_policy.h", "apex_decode.hip")]
+                  for f in ("kernels.h", "plan_policy.h")]
 
 
 def log(msg):
@@ -99,6 +106,89 @@ def cpu_baseline(wl, target_s):
     }
 
 
+def time_append(A, torch, k_new, v_new, k_cache, v_cache, slots, reps):
+    """Mean kernel time (ms) of apex_kv_append, from events around each call.
+
+    A short kernel finishes before the host can enqueue the next one, so the
+    stream is first held by a spin kernel while every (event, append, event)
+    triple is enqueued; the appends then run back to back and each event
+    pair brackets its kernel alone rather than the host's enqueue latency."""
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(reps)]
+    for _ in range(3):
+        A.kv_append(k_new, v_new, k_cache, v_cache, slots)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(20_000_000)
+    for a, b in pairs:
+        a.record()
+        A.kv_append(k_new, v_new, k_cache, v_cache, slots)
+        b.record()
+    torch.cuda.synchronize()
+    return sum(a.elapsed_time(b) for a, b in pairs) / reps
+
+
+def time_copy(torch, nbytes, reps):
+    """Mean time (ms) of a plain device copy of nbytes (reads and writes
+    nbytes each): the read+write bandwidth a scatter can hope for."""
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def append_bytes(tokens, Hkv, d):
+    return tokens * Hkv * d * 2 * 4 + tokens * 8
+
+
+def measure_append(A, torch, W, wl, reps):
+    cfg = wl.cfg
+    # the step's own append: rewrite each request's newest row with its
+    # current values, so the workload's cache is unchanged
+    slots_np = W.append_slots(wl.layout)
+    slots = torch.from_numpy(slots_np).cuda()
+    valid = slots_np >= 0
+    blk = torch.from_numpy(slots_np[valid] // cfg.block_size).cuda()
+    pos = torch.from_numpy(slots_np[valid] % cfg.block_size).cuda()
+    kn = torch.zeros((cfg.B, cfg.Hkv, cfg.d), dtype=torch.float16, device="cuda")
+    vn = torch.zeros_like(kn)
+    sel = torch.from_numpy(valid.nonzero()[0]).cuda()
+    kn[sel] = wl.k_cache[blk, :, pos, :]
+    vn[sel] = wl.v_cache[blk, :, pos, :]
+    ms = time_append(A, torch, kn, vn, wl.k_cache, wl.v_cache, slots, reps)
+    nb = append_bytes(int(valid.sum()), cfg.Hkv, cfg.d)
+    step = {"tokens": int(valid.sum()), "us_mean": round(ms * 1e3, 2), "bytes": nb,
+            "achieved": round(nb / (ms * 1e-3) / 1e9, 2)}
+    # prompt-sized bulk append into a pool of its own
+    T, pool = 65536, 4096
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(cfg.seed)
+    kc = torch.zeros((pool, cfg.Hkv, cfg.block_size, cfg.d), dtype=torch.float16, device="cuda")
+    vc = torch.zeros_like(kc)
+    kn = torch.randn((T, cfg.Hkv, cfg.d), generator=gen, device="cuda").half()
+    vn = torch.randn((T, cfg.Hkv, cfg.d), generator=gen, device="cuda").half()
+    perm = torch.randperm(pool, generator=gen, device="cuda")
+    slots = (perm[:, None] * cfg.block_size
+             + torch.arange(cfg.block_size, device="cuda")[None, :]).reshape(-1)[:T].contiguous()
+    ms = time_append(A, torch, kn, vn, kc, vc, slots, reps)
+    nb = append_bytes(T, cfg.Hkv, cfg.d)
+    achieved = nb / (ms * 1e-3) / 1e9
+    del kc, vc, kn, vn
+    copy_ms = time_copy(torch, nb // 2, reps)
+    bulk = {"tokens": T, "us_mean": round(ms * 1e3, 2), "bytes": nb, "bound": "hbm",
+            "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "device_copy_same_bytes_GBps": round(nb / (copy_ms * 1e-3) / 1e9, 2)}
+    return {"kernel": "kv_append_kernel", "decode_step": step, "bulk": bulk}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -115,6 +205,7 @@ def main():
                     help="only measure achievable HBM read bandwidth (stream and 4 KiB gather)")
     ap.add_argument("--probe-mib", type=int, default=4096,
                     help="buffer size of --hbm-probe in MiB")
+    ap.add_argument("--no-append", action="store_true", help="skip the kv_append lines")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -231,6 +322,9 @@ def main():
         },
         "cpu_baseline": None,
     }
+    if not args.no_append:
+        log("timing kv_append")
+        result["kv_append"] = measure_append(A, torch, W, wl, max(10, args.steps))
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)

@@ -6,10 +6,11 @@ If the built library is missing, importing the binding's functions raises --
 there is no fallback.
 
     out = decode_attention(q, k_cache, v_cache, block_table, context_lens, scale)
+    kv_append(k_new, v_new, k_cache, v_cache, slot_mapping)      # before the step
 
 q [B][Hq][128] fp16, caches [num_blocks][Hkv][16][128] fp16, block_table int32
 [B][stride], context_lens int32 [B] (all on the same GPU).  The names and
-argument order follow include/apex_decode.h.
+argument order follow include/apex_decode.h and include/apex_kv_append.h.
 """
 import ctypes
 import os
@@ -18,7 +19,7 @@ __all__ = [
     "ApexError", "LIB_PATH", "load_library", "decode_attention", "decode_attention_ex",
     "workspace_bytes", "plan_host", "last_error", "release_workspace", "version",
     "APEX_OK", "APEX_ERR_INVALID_ARG", "APEX_ERR_UNSUPPORTED", "APEX_ERR_OUT_OF_MEMORY",
-    "APEX_ERR_HIP", "EXPORTED_SYMBOLS", "counter_bytes",
+    "APEX_ERR_HIP", "EXPORTED_SYMBOLS", "counter_bytes", "kv_append",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libapex_decode.so")
@@ -32,7 +33,7 @@ APEX_ERR_HIP = -4
 EXPORTED_SYMBOLS = (
     "apex_decode_attention", "apex_decode_attention_ex", "apex_decode_workspace_bytes",
     "apex_decode_counter_bytes", "apex_decode_plan_host", "apex_decode_last_error",
-    "apex_decode_release_workspace", "apex_decode_version",
+    "apex_decode_release_workspace", "apex_decode_version", "apex_kv_append",
 )
 
 
@@ -96,6 +97,8 @@ def load_library(path=None):
     lib.apex_decode_release_workspace.argtypes = []
     lib.apex_decode_version.restype = i32
     lib.apex_decode_version.argtypes = []
+    lib.apex_kv_append.restype = i32
+    lib.apex_kv_append.argtypes = [vp, vp, i64, vp, vp, vp, i32, i32, i32, i32, i64, vp]
     if path is None:
         _LIB = lib
     return lib
@@ -226,3 +229,30 @@ def plan_host(context_lens, Hkv, launched_workers, block_size=16, forced=False):
     _check(rc)
     return {"contributors": contrib[:B * Hkv].reshape(B, Hkv), "units": units.value,
             "active": active.value, "partials": partials.value}
+
+
+def kv_append(k_new, v_new, k_cache, v_cache, slot_mapping, stream=None):
+    """apex_kv_append over torch tensors (in place on the caches).
+
+    k_new/v_new: fp16 [T][Hkv][d] with unit strides inside a token (the token
+    stride may be wider, e.g. views into a fused QKV buffer, but must be the
+    same for both); caches [num_blocks][Hkv][block_size][d]; slot_mapping
+    int64 [T] (negative = padding)."""
+    if k_new.dim() != 3 or v_new.shape != k_new.shape or k_cache.dim() != 4:
+        raise ValueError("k_new/v_new must be [T][Hkv][d]; caches [num_blocks][Hkv][block_size][d]")
+    T, Hkv, d = k_new.shape
+    nb, hkv2, bs, d2 = k_cache.shape
+    if (hkv2, d2) != (Hkv, d) or v_cache.shape != k_cache.shape:
+        raise ValueError("new rows and caches disagree on Hkv or d")
+    for t in (k_new, v_new):
+        if t.stride(2) != 1 or t.stride(1) != d:
+            raise ValueError("each token's rows must be contiguous [Hkv][d]")
+    if T > 1 and k_new.stride(0) != v_new.stride(0):
+        raise ValueError("k_new and v_new must share the token stride")
+    if not (k_cache.is_contiguous() and v_cache.is_contiguous() and slot_mapping.is_contiguous()):
+        raise ValueError("caches and slot_mapping must be contiguous")
+    stride = k_new.stride(0) if T > 1 else 0
+    rc = load_library().apex_kv_append(_ptr(k_new), _ptr(v_new), stride, _ptr(k_cache),
+                                       _ptr(v_cache), _ptr(slot_mapping), T, Hkv, d, bs, nb,
+                                       _stream_handle(stream, k_cache.device))
+    _check(rc)

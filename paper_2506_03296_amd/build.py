@@ -7,11 +7,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libapex_decode.so")
-SOURCES = [os.path.join(CSRC, "apex_decode.hip")]
+SOURCES = [os.path.join(CSRC, "apex_decode.hip"), os.path.join(CSRC, "kv_append.hip")]
 PROBE_LIB = os.path.join(HERE, "libapex_hbm_probe.so")
 PROBE_SOURCES = [os.path.join(CSRC, "hbm_probe.hip")]
 HEADERS = [os.path.join(ROOT, "include", "apex_decode.h"),
-           os.path.join(CSRC, "kernels.h"), os.path.join(CSRC, "plan_policy.h")]
+           os.path.join(ROOT, "include", "apex_kv_append.h"),
+           os.path.join(CSRC, "kernels.h"), os.path.join(CSRC, "plan_policy.h"),
+           os.path.join(CSRC, "status.h")]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -15,10 +15,13 @@
 #include "apex_decode.h"
 #include "kernels.h"
 #include "plan_policy.h"
+#include "status.h"
+
+namespace apex {
 
 namespace {
-
 thread_local char g_last_error[512] = "";
+}
 
 int fail(int code, const char* fmt, ...)
 {
@@ -28,6 +31,16 @@ int fail(int code, const char* fmt, ...)
     va_end(ap);
     return code;
 }
+
+void clear_error() { g_last_error[0] = 0; }
+
+const char* last_error_message() { return g_last_error; }
+
+}  // namespace apex
+
+namespace {
+
+using apex::fail;
 
 constexpr int kMaxDevices = 64;
 constexpr int kGroupKinds = 4;   // G = 1, 2, 4, 8
@@ -174,7 +187,7 @@ extern "C" {
 
 int apex_decode_version(void) { return 200; }
 
-const char* apex_decode_last_error(void) { return g_last_error; }
+const char* apex_decode_last_error(void) { return apex::last_error_message(); }
 
 size_t apex_decode_counter_bytes(int B, int Hkv)
 {
@@ -198,7 +211,7 @@ int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block
                           int launched_workers, int forced, int32_t* contributors_out,
                           int64_t* units_out, int64_t* active_out, int64_t* partials_out)
 {
-    g_last_error[0] = 0;
+    apex::clear_error();
     if (B < 0 || Hkv <= 0 || launched_workers <= 0)
         return fail(APEX_ERR_INVALID_ARG, "bad partition arguments");
     if (B > 0 && !context_lens) return fail(APEX_ERR_INVALID_ARG, "context_lens is NULL");
@@ -231,7 +244,7 @@ int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block
 
 int apex_decode_attention_ex(const apex_decode_args* args)
 {
-    g_last_error[0] = 0;
+    apex::clear_error();
     if (!args) return fail(APEX_ERR_INVALID_ARG, "args is NULL");
     const apex_decode_args& a = *args;
     int rc = check_shapes(a.B, a.Hq, a.Hkv, a.d, a.block_size);
@@ -337,7 +350,7 @@ int apex_decode_attention(const void* q, const void* k_cache, const void* v_cach
 
 int apex_decode_release_workspace(void)
 {
-    g_last_error[0] = 0;
+    apex::clear_error();
     std::lock_guard<std::mutex> lock(g_mutex);
     int rc = APEX_OK;
     for (int d = 0; d < kMaxDevices; ++d) {

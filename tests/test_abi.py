@@ -12,6 +12,7 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "apex_decode.h")
+LIB_HEADERS = [HEADER, os.path.join(ROOT, "include", "apex_kv_append.h")]
 
 A = pytest.importorskip("paper_2506_03296_amd")
 
@@ -25,9 +26,11 @@ def lib():
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(apex_\w+)\s*\(", text)))
+    names = set()
+    for h in LIB_HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(apex_\w+)\s*\(", text))
+    return sorted(names)
 
 
 def test_header_declares_the_base_entry_point_with_its_argument_order():
@@ -209,3 +212,60 @@ def test_plan_host_rejects_bad_arguments(lib):
 def test_counter_bytes(lib):
     assert A.counter_bytes(512, 8) == 512 * 8 * 4
     assert A.counter_bytes(3, 1) == 256
+
+
+# ---------------------------------------------------------------------------
+# KV append: argument validation (returns before any HIP call)
+# ---------------------------------------------------------------------------
+
+def append_call(lib, T=4, Hkv=8, d=128, bs=16, nb=100, stride=0, kn=FAKE, vn=FAKE + (1 << 30),
+                kc=FAKE + (2 << 30), vc=FAKE + (3 << 30), slots=FAKE + (4 << 30)):
+    return lib.apex_kv_append(kn, vn, stride, kc, vc, slots, T, Hkv, d, bs, nb, None)
+
+
+def test_kv_append_header_argument_order():
+    text = open(LIB_HEADERS[1]).read()
+    sig = re.search(r"int apex_kv_append\((.*?)\);", text, flags=re.S).group(1)
+    names = [re.findall(r"(\w+)\s*$", p.strip())[0] for p in sig.split(",")]
+    assert names == ["k_new", "v_new", "new_token_stride", "k_cache", "v_cache", "slot_mapping",
+                     "T", "Hkv", "d", "block_size", "num_blocks", "stream"]
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(T=-1), A.APEX_ERR_INVALID_ARG),
+    (dict(Hkv=0), A.APEX_ERR_INVALID_ARG),
+    (dict(bs=0), A.APEX_ERR_INVALID_ARG),
+    (dict(nb=-1), A.APEX_ERR_INVALID_ARG),
+    (dict(d=12), A.APEX_ERR_UNSUPPORTED),
+    (dict(d=4096), A.APEX_ERR_UNSUPPORTED),
+    (dict(stride=8 * 128 - 8), A.APEX_ERR_INVALID_ARG),
+    (dict(stride=8 * 128 + 4), A.APEX_ERR_INVALID_ARG),
+    (dict(T=1 << 28, Hkv=16), A.APEX_ERR_UNSUPPORTED),
+    (dict(nb=1 << 50), A.APEX_ERR_INVALID_ARG),
+    (dict(kn=0), A.APEX_ERR_INVALID_ARG),
+    (dict(slots=0), A.APEX_ERR_INVALID_ARG),
+    (dict(kn=FAKE + 8), A.APEX_ERR_INVALID_ARG),
+    (dict(vc=FAKE + (3 << 30) + 2), A.APEX_ERR_INVALID_ARG),
+    (dict(slots=FAKE + (4 << 30) + 4), A.APEX_ERR_INVALID_ARG),
+    (dict(vc=FAKE + (2 << 30) + 4096), A.APEX_ERR_INVALID_ARG),     # caches overlap
+    (dict(kn=FAKE + (2 << 30) + 256), A.APEX_ERR_INVALID_ARG),      # input inside a cache
+    (dict(slots=FAKE + (3 << 30)), A.APEX_ERR_INVALID_ARG),         # slots inside a cache
+])
+def test_kv_append_invalid_arguments_are_rejected(lib, kw, code):
+    assert append_call(lib, **kw) == code
+    assert A.last_error() != ""
+
+
+def test_kv_append_empty_or_poolless_calls_are_noops(lib):
+    assert append_call(lib, T=0, kn=0, vn=0, kc=0, vc=0, slots=0) == A.APEX_OK
+    assert A.last_error() == ""
+    assert append_call(lib, nb=0) == A.APEX_OK
+
+
+def test_kv_append_overlapping_fused_inputs_are_allowed(lib):
+    # K and V views into one fused [T][Hq + 2 Hkv][d] buffer interleave
+    d, Hq, Hkv = 128, 32, 8
+    stride = (Hq + 2 * Hkv) * d
+    base = FAKE
+    kn, vn = base + Hq * d * 2, base + (Hq + Hkv) * d * 2
+    assert append_call(lib, T=4, nb=0, stride=stride, kn=kn, vn=vn) == A.APEX_OK
