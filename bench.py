@@ -16,6 +16,9 @@ JSON line:
              when it was taken on the current kernel source, else null
   cpu_baseline  the fp64 CPU oracle on the host cores over a bounded sample of
              the same workload (the first requests), in the same unit
+  cpu_attention  the library's own host backend (libapex_cpu.so, SIMD +
+             thread pool) on a host copy of the same workload, against the
+             host read bandwidth measured with the same threads
   kv_append  the paged KV append that precedes each step (apex_kv_append),
              timed alone with events around its kernel: the step's own append
              (one token per request at position L_b - 1 of the workload's
@@ -189,6 +192,31 @@ def measure_append(A, torch, W, wl, reps):
     return {"kernel": "kv_append_kernel", "decode_step": step, "bulk": bulk}
 
 
+def measure_cpu_attention(wl, threads, reps=5):
+    """The host backend over a host copy of the whole workload."""
+    from paper_2506_03296_amd import cpu
+    cpu.set_threads(threads)
+    q = wl.q.cpu().numpy()
+    k = wl.k_cache.cpu().numpy()
+    v = wl.v_cache.cpu().numpy()
+    bt = wl.block_table.cpu().numpy()
+    lens = wl.context_lens.cpu().numpy()
+    out = cpu.decode_attention(q, k, v, bt, lens, wl.scale)
+    best = float("inf")
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        cpu.decode_attention(q, k, v, bt, lens, wl.scale, out=out)
+        best = min(best, time.perf_counter() - t0)
+    del k, v
+    read = cpu.read_bandwidth(1 << 30, num_threads=threads, reps=3)
+    achieved = wl.algorithmic_bytes / best / 1e9
+    return {"kernel": "apex_cpu_decode_attention", "isa": {2: "avx512", 1: "avx2"}.get(cpu.isa(), "none"),
+            "threads": threads, "us_per_layer_step": round(best * 1e6, 1),
+            "bound": "host-dram", "achieved": round(achieved, 2), "unit": "GB/s",
+            "host_read_GBps": round(read, 2), "frac_of_host_read": round(achieved / read, 4),
+            "timing": f"best of {reps} calls, wall clock"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -206,6 +234,8 @@ def main():
     ap.add_argument("--probe-mib", type=int, default=4096,
                     help="buffer size of --hbm-probe in MiB")
     ap.add_argument("--no-append", action="store_true", help="skip the kv_append lines")
+    ap.add_argument("--no-cpu-attention", action="store_true",
+                    help="skip the host backend line")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -322,6 +352,10 @@ def main():
         },
         "cpu_baseline": None,
     }
+    if not args.no_cpu_attention:
+        log("timing the host backend")
+        threads = max(1, min(16, len(os.sched_getaffinity(0))))
+        result["cpu_attention"] = measure_cpu_attention(wl, threads)
     if not args.no_append:
         log("timing kv_append")
         result["kv_append"] = measure_append(A, torch, W, wl, max(10, args.steps))

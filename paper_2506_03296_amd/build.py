@@ -2,12 +2,15 @@
 import os
 import subprocess
 import sys
+import tempfile
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libapex_decode.so")
 SOURCES = [os.path.join(CSRC, "apex_decode.hip"), os.path.join(CSRC, "kv_append.hip")]
+CPU_LIB = os.path.join(HERE, "libapex_cpu.so")
+CPU_DIR = os.path.join(CSRC, "cpu")
 PROBE_LIB = os.path.join(HERE, "libapex_hbm_probe.so")
 PROBE_SOURCES = [os.path.join(CSRC, "hbm_probe.hip")]
 HEADERS = [os.path.join(ROOT, "include", "apex_decode.h"),
@@ -34,8 +37,41 @@ def _compile(sources, out, extra, quiet):
     return out
 
 
+CXX_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall", "-Wextra", "-Wno-unused-parameter",
+             "-I", os.path.join(ROOT, "include"), "-I", CPU_DIR]
+ISA_FLAGS = {
+    "simd_avx512": ["-mavx512f", "-mavx512bw", "-mavx512vl", "-mavx512dq", "-mf16c", "-mfma"],
+    "simd_avx2": ["-mavx2", "-mfma", "-mf16c"],
+}
+
+
+def _run(cmd, quiet):
+    if not quiet:
+        print(" ".join(cmd), flush=True)
+    subprocess.check_call(cmd)
+
+
+def build_cpu(out=CPU_LIB, quiet=False):
+    """Compile the host paged-attention backend (g++, baseline x86-64 host
+    code plus one object per SIMD instruction set)."""
+    cxx = os.environ.get("CXX", "g++")
+    with tempfile.TemporaryDirectory() as tmp:
+        objs = []
+        for ns, flags in ISA_FLAGS.items():
+            obj = os.path.join(tmp, f"attend_{ns}.o")
+            _run([cxx, *CXX_FLAGS, *flags, f"-DAPEX_SIMD_NS={ns}", "-c",
+                  os.path.join(CPU_DIR, "attend_simd.cpp"), "-o", obj], quiet)
+            objs.append(obj)
+        _run([cxx, *CXX_FLAGS, "-shared", "-pthread", os.path.join(CPU_DIR, "cpu_attention.cpp"),
+              *objs, "-o", out + ".tmp"], quiet)
+    os.replace(out + ".tmp", out)
+    return out
+
+
 def build(out=LIB, extra=(), quiet=False):
-    """Compile the decode-attention library and the HBM probe library."""
+    """Compile the decode-attention library, the host attention backend and
+    the HBM probe library."""
+    build_cpu(quiet=quiet)
     _compile(PROBE_SOURCES, PROBE_LIB, extra, quiet)
     return _compile(SOURCES, out, extra, quiet)
 
