@@ -113,3 +113,45 @@ def main_scheduler(p_in, d_gpu_in, d_cpu_in, asym_pipe_strat, selection_inputs):
         return ASYNC_OVERLAP
     kw = selection_inputs(p_sch, d_gpu_sch, d_cpu_sch)
     return strategy_selection(prefill=len(p_sch) > 0, **kw)[0]
+
+
+# ---------------------------------------------------------------------------
+# profiled inputs (Sec. 3.2 "Parameter Estimation via Offline Profiling"):
+# times measured at sample points, read between them by linear interpolation
+# ---------------------------------------------------------------------------
+
+def interp1(xs, ys, x):
+    """Piecewise-linear through (xs[i], ys[i]) (xs strictly increasing),
+    extended past either end along the nearest segment, never below 0.
+    A single sample is a constant."""
+    n = len(xs)
+    if n == 1:
+        return max(ys[0], 0.0)
+    i = 0
+    while i < n - 2 and x > xs[i + 1]:
+        i += 1
+    y = ys[i] + (ys[i + 1] - ys[i]) * (x - xs[i]) / (xs[i + 1] - xs[i])
+    return max(y, 0.0)
+
+
+def interp2(bs, ts, table, b, t):
+    """Bilinear over a batch x tokens grid (table[i][j] at bs[i], ts[j]),
+    extended like interp1 along each axis."""
+    rows = [interp1(ts, table[i], t) for i in range(len(bs))]
+    return interp1(bs, rows, b)
+
+
+def inputs_from_profile(profile, gpu_batch, gpu_tokens, cpu_batch, cpu_tokens, prefill_tokens=0.0):
+    """Rates and times for strategy_selection from a profile dict:
+    gatt_tokens/gatt_seconds, glin_batch/glin_seconds, cpu_batch/cpu_tokens/
+    cpu_seconds (grid), pref_tokens/pref_linear_seconds/pref_attn_seconds.
+    N_G = GPU tokens / T_gatt(GPU tokens); N_C = CPU tokens / T_cpu(batch, tokens)."""
+    t_gatt = interp1(profile["gatt_tokens"], profile["gatt_seconds"], gpu_tokens)
+    t_glinear = interp1(profile["glin_batch"], profile["glin_seconds"], gpu_batch)
+    t_cpu = interp2(profile["cpu_batch"], profile["cpu_tokens"], profile["cpu_seconds"], cpu_batch, cpu_tokens)
+    out = dict(n_g=gpu_tokens / t_gatt, n_c=cpu_tokens / t_cpu if cpu_tokens > 0 else 0.0,
+               t_glinear=t_glinear, t_gatt=t_gatt)
+    if prefill_tokens > 0:
+        out["t_glinear_pref"] = interp1(profile["pref_tokens"], profile["pref_linear_seconds"], prefill_tokens)
+        out["t_gatt_pref"] = interp1(profile["pref_tokens"], profile["pref_attn_seconds"], prefill_tokens)
+    return out

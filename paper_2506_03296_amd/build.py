@@ -63,7 +63,7 @@ def build_cpu(out=CPU_LIB, quiet=False):
                   os.path.join(CPU_DIR, "attend_simd.cpp"), "-o", obj], quiet)
             objs.append(obj)
         _run([cxx, *CXX_FLAGS, "-shared", "-pthread", os.path.join(CPU_DIR, "cpu_attention.cpp"),
-              *objs, "-o", out + ".tmp"], quiet)
+              os.path.join(CSRC, "sched", "scheduler.cpp"), *objs, "-o", out + ".tmp"], quiet)
     os.replace(out + ".tmp", out)
     return out
 

@@ -38,6 +38,22 @@ __attribute__((format(printf, 2, 3))) int fail(int code, const char* fmt, ...)
     return code;
 }
 
+}  // namespace
+
+namespace apex_cpu {
+// error reporting shared with the scheduler (scheduler.cpp)
+__attribute__((visibility("hidden"), format(printf, 2, 3))) int sched_fail(int code, const char* fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return code;
+}
+}  // namespace apex_cpu
+
+namespace {
+
 constexpr int kMaxD = 512;
 constexpr int kMaxG = 64;
 constexpr int kDefaultMinChunk = 512;

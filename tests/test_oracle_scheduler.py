@@ -193,3 +193,42 @@ def test_planted_mistakes_are_caught():
     assert _pins_pass(S)
     for name in MUTANTS:
         assert not _pins_pass(_mutant(name)), f"planted mistake '{name}' passed every pin"
+
+
+# ---------------------------------------------------------------------------
+# profile interpolation
+# ---------------------------------------------------------------------------
+
+def test_interp1_hits_samples_is_linear_between_and_extends_the_end_segments():
+    xs = [F(1), F(4), F(10)]
+    ys = [F(2), F(8), F(11)]
+    for x, y in zip(xs, ys):
+        assert S.interp1(xs, ys, x) == y
+    assert S.interp1(xs, ys, F(2)) == F(4)                  # slope 2 on [1, 4]
+    assert S.interp1(xs, ys, F(7)) == F(19, 2)              # slope 1/2 on [4, 10]
+    assert S.interp1(xs, ys, F(12)) == F(12)                # extended right
+    assert S.interp1(xs, ys, F(0)) == F(0)                  # extended left: 2 - 2 = 0
+    assert S.interp1(xs, ys, F(-5)) == 0                    # never below zero
+    assert S.interp1([F(3)], [F(5)], F(100)) == 5           # one sample: constant
+
+
+def test_interp2_is_bilinear_on_the_grid():
+    bs, ts = [F(1), F(3)], [F(10), F(20)]
+    table = [[F(1), F(3)], [F(5), F(11)]]
+    assert S.interp2(bs, ts, table, F(1), F(10)) == 1
+    assert S.interp2(bs, ts, table, F(3), F(20)) == 11
+    # centre: mean of the four corners for a bilinear patch
+    assert S.interp2(bs, ts, table, F(2), F(15)) == F(1 + 3 + 5 + 11, 4)
+
+
+def test_inputs_from_profile_rates():
+    prof = dict(gatt_tokens=[F(1000), F(2000)], gatt_seconds=[F(1, 100), F(2, 100)],
+                glin_batch=[F(1), F(100)], glin_seconds=[F(1, 1000), F(100, 1000)],
+                cpu_batch=[F(1), F(10)], cpu_tokens=[F(100), F(1000)],
+                cpu_seconds=[[F(1), F(10)], [F(2), F(20)]],
+                pref_tokens=[F(10), F(20)], pref_linear_seconds=[F(1), F(2)], pref_attn_seconds=[F(3), F(4)])
+    kw = S.inputs_from_profile(prof, F(50), F(1500), F(1), F(100), prefill_tokens=F(15))
+    assert kw["t_gatt"] == F(15, 1000) and kw["n_g"] == F(1500) / F(15, 1000)
+    assert kw["t_glinear"] == F(50, 1000)
+    assert kw["n_c"] == F(100)
+    assert kw["t_glinear_pref"] == F(3, 2) and kw["t_gatt_pref"] == F(7, 2)
