@@ -19,6 +19,14 @@ JSON line:
   cpu_attention  the library's own host backend (libapex_cpu.so, SIMD +
              thread pool) on a host copy of the same workload, against the
              host read bandwidth measured with the same threads
+  overlap    the Asynchronous Overlap runtime (libapex_overlap.so) in a
+             synthetic decode iteration of 8 Llama-3.1-8B layers: bf16
+             linears on the unified batch, this workload's attention on the
+             GPU, 16 extra requests attended on the host; iteration time
+             GPU-only (without the extra requests; and with their rows in
+             the linears but no attention for them, the floor of the
+             overlap), with the overlap (results collected one iteration
+             later) and with a blocking wait in every layer
   kv_append  the paged KV append that precedes each step (apex_kv_append),
              timed alone with events around its kernel: the step's own append
              (one token per request at position L_b - 1 of the workload's
@@ -217,6 +225,109 @@ def measure_cpu_attention(wl, threads, reps=5):
             "timing": f"best of {reps} calls, wall clock"}
 
 
+def measure_overlap(A, torch, wl, layers=8, b_cpu=16, l_cpu=512, iters=6, warmup=2):
+    """Iteration times of a synthetic decode loop with and without host
+    attention for b_cpu extra requests (see the module docstring)."""
+    import numpy as np
+
+    from paper_2506_03296_amd import cpu, overlap
+    from paper_2506_03296_amd.profiler import layer_linears
+    # leave cores to the thread that launches the GPU work
+    threads = max(1, min(8, len(os.sched_getaffinity(0)) // 2))
+    cpu.set_threads(threads)
+    cfg = wl.cfg
+    total = warmup + iters
+    stride = -(-(l_cpu + total + 1) // cfg.block_size) + 1
+    num_blocks = b_cpu * stride
+    table = np.arange(num_blocks, dtype=np.int32).reshape(b_cpu, stride)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(cfg.seed + 1)
+    q_c = torch.randn((b_cpu, cfg.Hq, cfg.d), generator=gen, device="cuda").half()
+    kn = torch.randn((b_cpu, cfg.Hkv, cfg.d), generator=gen, device="cuda").half()
+    vn = torch.randn((b_cpu, cfg.Hkv, cfg.d), generator=gen, device="cuda").half()
+    outs = [torch.empty_like(q_c) for _ in range(layers)]
+    lin_gpu = layer_linears(torch, cfg.B, seed=1)
+    lin_all = layer_linears(torch, cfg.B + b_cpu, seed=2)
+
+    def attn():
+        A.decode_attention_ex(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens,
+                              wl.scale, out=wl.out)
+
+    # the host attention alone, for reference
+    hk = np.zeros((num_blocks, cfg.Hkv, cfg.block_size, cfg.d), np.float16)
+    lens0 = np.full(b_cpu, l_cpu, np.int32)
+    qh = q_c.cpu().numpy()
+    cpu.decode_attention(qh, hk, hk, table, lens0, wl.scale)
+    t_cpu = min(_timed(lambda: cpu.decode_attention(qh, hk, hk, table, lens0, wl.scale))
+                for _ in range(5))
+
+    times, waits = {}, {}
+    for mode in ("gpu_only", "gpu_only_unified", "async_overlap", "sync_wait"):
+        rt = overlap.Overlap(layers, b_cpu, cfg.Hq, cfg.Hkv, cfg.d, cfg.block_size, wl.scale,
+                             num_blocks, stride, threads=threads)
+        lens = np.full(b_cpu, l_cpu - 1, np.int32)
+        prev = [None] * layers
+        n_wait = 0
+
+        def iteration():
+            nonlocal lens, n_wait
+            lens = lens + 1
+            pos = lens - 1
+            slots = table[np.arange(b_cpu), pos // cfg.block_size].astype(np.int64) * cfg.block_size \
+                + pos % cfg.block_size
+            for l in range(layers):
+                if mode.startswith("gpu_only"):
+                    (lin_gpu if mode == "gpu_only" else lin_all)()
+                    attn()
+                    continue
+                lin_all()
+                t = rt.submit(l, q_c, kn, vn, slots, table, lens)
+                attn()
+                if mode == "sync_wait":
+                    rt.wait(t, outs[l])
+                    continue
+                if prev[l] is not None and not rt.poll(prev[l], outs[l]):
+                    n_wait += 1
+                    rt.wait(prev[l], outs[l])
+                prev[l] = t
+
+        for _ in range(warmup):
+            iteration()
+        torch.cuda.synchronize()
+        n_wait = 0
+        t0 = time.perf_counter()
+        for _ in range(iters):
+            iteration()
+        torch.cuda.synchronize()
+        times[mode] = (time.perf_counter() - t0) / iters
+        waits[mode] = n_wait
+        for l in range(layers):
+            if prev[l] is not None:
+                rt.wait(prev[l], outs[l])
+        torch.cuda.synchronize()
+        rt.close()
+    tok = {"gpu_only": cfg.B, "gpu_only_unified": cfg.B, "async_overlap": cfg.B + b_cpu,
+           "sync_wait": cfg.B + b_cpu}
+    return {
+        "runtime": "apex_overlap", "layers": layers, "gpu_requests": cfg.B, "cpu_requests": b_cpu,
+        "cpu_context_tokens": l_cpu, "host_threads": threads,
+        "iteration_ms": {k: round(v * 1e3, 3) for k, v in times.items()},
+        "tokens_per_s": {k: round(tok[k] / v, 1) for k, v in times.items()},
+        "host_attention_ms_per_layer": round(t_cpu * 1e3, 3),
+        "overlap_waits": waits["async_overlap"],
+        "overlap_cost_ms": round((times["async_overlap"] - times["gpu_only_unified"]) * 1e3, 3),
+        "hidden_fraction": round(max(0.0, times["sync_wait"] - times["async_overlap"])
+                                 / (layers * t_cpu), 3),
+        "timing": f"wall clock over {iters} iterations after {warmup}",
+    }
+
+
+def _timed(fn):
+    t0 = time.perf_counter()
+    fn()
+    return time.perf_counter() - t0
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -236,6 +347,7 @@ def main():
     ap.add_argument("--no-append", action="store_true", help="skip the kv_append lines")
     ap.add_argument("--no-cpu-attention", action="store_true",
                     help="skip the host backend line")
+    ap.add_argument("--no-overlap", action="store_true", help="skip the overlap runtime line")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -356,6 +468,9 @@ def main():
         log("timing the host backend")
         threads = max(1, min(16, len(os.sched_getaffinity(0))))
         result["cpu_attention"] = measure_cpu_attention(wl, threads)
+    if not args.no_overlap:
+        log("timing the overlap runtime")
+        result["overlap"] = measure_overlap(A, torch, wl)
     if not args.no_append:
         log("timing kv_append")
         result["kv_append"] = measure_append(A, torch, W, wl, max(10, args.steps))

@@ -64,7 +64,8 @@ typedef enum apex_status {
     APEX_ERR_INVALID_ARG = -1,   /* null/misaligned pointer, B < 0, Hq % Hkv != 0, aliasing */
     APEX_ERR_UNSUPPORTED = -2,   /* d, block_size or group size outside the supported set */
     APEX_ERR_OUT_OF_MEMORY = -3, /* workspace allocation failed or caller workspace too small */
-    APEX_ERR_HIP = -4            /* a HIP runtime call or kernel launch failed */
+    APEX_ERR_HIP = -4,           /* a HIP runtime call or kernel launch failed */
+    APEX_ERR_BUSY = -5           /* a resource is still in use (apex_overlap.h: result slot) */
 } apex_status;
 
 /*

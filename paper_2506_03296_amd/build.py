@@ -11,6 +11,8 @@ LIB = os.path.join(HERE, "libapex_decode.so")
 SOURCES = [os.path.join(CSRC, "apex_decode.hip"), os.path.join(CSRC, "kv_append.hip")]
 CPU_LIB = os.path.join(HERE, "libapex_cpu.so")
 CPU_DIR = os.path.join(CSRC, "cpu")
+OVERLAP_LIB = os.path.join(HERE, "libapex_overlap.so")
+OVERLAP_SOURCES = [os.path.join(CSRC, "overlap", "overlap.hip")]
 PROBE_LIB = os.path.join(HERE, "libapex_hbm_probe.so")
 PROBE_SOURCES = [os.path.join(CSRC, "hbm_probe.hip")]
 HEADERS = [os.path.join(ROOT, "include", "apex_decode.h"),
@@ -69,10 +71,13 @@ def build_cpu(out=CPU_LIB, quiet=False):
 
 
 def build(out=LIB, extra=(), quiet=False):
-    """Compile the decode-attention library, the host attention backend and
-    the HBM probe library."""
+    """Compile the decode-attention library, the host attention backend, the
+    overlap runtime (linked against the host backend) and the HBM probe
+    library."""
     build_cpu(quiet=quiet)
     _compile(PROBE_SOURCES, PROBE_LIB, extra, quiet)
+    _compile(OVERLAP_SOURCES, OVERLAP_LIB,
+             [*extra, "-L", HERE, "-lapex_cpu", "-Wl,-rpath,$ORIGIN", "-pthread"], quiet)
     return _compile(SOURCES, out, extra, quiet)
 
 
