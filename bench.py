@@ -26,7 +26,10 @@ JSON line:
              GPU-only (without the extra requests; and with their rows in
              the linears but no attention for them, the floor of the
              overlap), with the overlap (results collected one iteration
-             later) and with a blocking wait in every layer
+             later by a readiness check that never blocks; a result not yet
+             ready is checked again in the next iteration and waited for
+             only if still missing then) and with a blocking wait in every
+             layer
   kv_append  the paged KV append that precedes each step (apex_kv_append),
              timed alone with events around its kernel: the step's own append
              (one token per request at position L_b - 1 of the workload's
@@ -225,7 +228,7 @@ def measure_cpu_attention(wl, threads, reps=5):
             "timing": f"best of {reps} calls, wall clock"}
 
 
-def measure_overlap(A, torch, wl, layers=8, b_cpu=16, l_cpu=512, iters=6, warmup=2):
+def measure_overlap(A, torch, wl, layers=8, b_cpu=16, l_cpu=512, iters=16, warmup=3):
     """Iteration times of a synthetic decode loop with and without host
     attention for b_cpu extra requests (see the module docstring)."""
     import numpy as np
@@ -242,9 +245,12 @@ def measure_overlap(A, torch, wl, layers=8, b_cpu=16, l_cpu=512, iters=6, warmup
     table = np.arange(num_blocks, dtype=np.int32).reshape(b_cpu, stride)
     gen = torch.Generator(device="cuda")
     gen.manual_seed(cfg.seed + 1)
-    q_c = torch.randn((b_cpu, cfg.Hq, cfg.d), generator=gen, device="cuda").half()
-    kn = torch.randn((b_cpu, cfg.Hkv, cfg.d), generator=gen, device="cuda").half()
-    vn = torch.randn((b_cpu, cfg.Hkv, cfg.d), generator=gen, device="cuda").half()
+    # the host-attended requests' new rows, q | k | v back to back (one copy)
+    nq, nkv = b_cpu * cfg.Hq * cfg.d, b_cpu * cfg.Hkv * cfg.d
+    rows = torch.randn((nq + 2 * nkv,), generator=gen, device="cuda").half()
+    q_c = rows[:nq].view(b_cpu, cfg.Hq, cfg.d)
+    kn = rows[nq:nq + nkv].view(b_cpu, cfg.Hkv, cfg.d)
+    vn = rows[nq + nkv:].view(b_cpu, cfg.Hkv, cfg.d)
     outs = [torch.empty_like(q_c) for _ in range(layers)]
     lin_gpu = layer_linears(torch, cfg.B, seed=1)
     lin_all = layer_linears(torch, cfg.B + b_cpu, seed=2)
@@ -261,16 +267,17 @@ def measure_overlap(A, torch, wl, layers=8, b_cpu=16, l_cpu=512, iters=6, warmup
     t_cpu = min(_timed(lambda: cpu.decode_attention(qh, hk, hk, table, lens0, wl.scale))
                 for _ in range(5))
 
-    times, waits = {}, {}
+    times, late, stalls = {}, {}, {}
     for mode in ("gpu_only", "gpu_only_unified", "async_overlap", "sync_wait"):
+        # three result slots per layer: one in flight, one collected late
         rt = overlap.Overlap(layers, b_cpu, cfg.Hq, cfg.Hkv, cfg.d, cfg.block_size, wl.scale,
-                             num_blocks, stride, threads=threads)
+                             num_blocks, stride, threads=threads, slots_per_layer=3)
         lens = np.full(b_cpu, l_cpu - 1, np.int32)
-        prev = [None] * layers
-        n_wait = 0
+        pending = [[] for _ in range(layers)]   # tickets not yet collected, oldest first
+        counts = {"late": 0, "stall": 0}
 
         def iteration():
-            nonlocal lens, n_wait
+            nonlocal lens
             lens = lens + 1
             pos = lens - 1
             slots = table[np.arange(b_cpu), pos // cfg.block_size].astype(np.int64) * cfg.block_size \
@@ -281,29 +288,35 @@ def measure_overlap(A, torch, wl, layers=8, b_cpu=16, l_cpu=512, iters=6, warmup
                     attn()
                     continue
                 lin_all()
+                if mode == "async_overlap" and len(pending[l]) == 2:
+                    # a result already one iteration late: it must be in now
+                    counts["stall"] += 1
+                    rt.wait(pending[l].pop(0), outs[l])
                 t = rt.submit(l, q_c, kn, vn, slots, table, lens)
                 attn()
                 if mode == "sync_wait":
                     rt.wait(t, outs[l])
                     continue
-                if prev[l] is not None and not rt.poll(prev[l], outs[l]):
-                    n_wait += 1
-                    rt.wait(prev[l], outs[l])
-                prev[l] = t
+                # readiness check of earlier results, never blocking: a result
+                # that is not ready is checked again in the next iteration
+                while pending[l] and rt.poll(pending[l][0], outs[l]):
+                    pending[l].pop(0)
+                counts["late"] += len(pending[l])
+                pending[l].append(t)
 
         for _ in range(warmup):
             iteration()
         torch.cuda.synchronize()
-        n_wait = 0
+        counts["late"] = counts["stall"] = 0
         t0 = time.perf_counter()
         for _ in range(iters):
             iteration()
         torch.cuda.synchronize()
         times[mode] = (time.perf_counter() - t0) / iters
-        waits[mode] = n_wait
+        late[mode], stalls[mode] = counts["late"], counts["stall"]
         for l in range(layers):
-            if prev[l] is not None:
-                rt.wait(prev[l], outs[l])
+            for t in pending[l]:
+                rt.wait(t, outs[l])
         torch.cuda.synchronize()
         rt.close()
     tok = {"gpu_only": cfg.B, "gpu_only_unified": cfg.B, "async_overlap": cfg.B + b_cpu,
@@ -314,7 +327,7 @@ def measure_overlap(A, torch, wl, layers=8, b_cpu=16, l_cpu=512, iters=6, warmup
         "iteration_ms": {k: round(v * 1e3, 3) for k, v in times.items()},
         "tokens_per_s": {k: round(tok[k] / v, 1) for k, v in times.items()},
         "host_attention_ms_per_layer": round(t_cpu * 1e3, 3),
-        "overlap_waits": waits["async_overlap"],
+        "late_results": late["async_overlap"], "stalls": stalls["async_overlap"],
         "overlap_cost_ms": round((times["async_overlap"] - times["gpu_only_unified"]) * 1e3, 3),
         "hidden_fraction": round(max(0.0, times["sync_wait"] - times["async_overlap"])
                                  / (layers * t_cpu), 3),

@@ -23,6 +23,8 @@
  *
  * Device buffers (on the current device, fp16, contiguous):
  *   q [B][Hq][d]; k_new, v_new [B][Hkv][d] (this token's rows); out [B][Hq][d]
+ *   When k_new starts right after q's B rows and v_new right after k_new's,
+ *   the three are copied to the host as one transfer.
  * Host arrays (copied at submit, the caller may reuse them at once):
  *   slot_mapping int64 [B] (host cache slot of the new token: block *
  *   block_size + position, negative = no append), block_table int32

@@ -42,8 +42,8 @@ __attribute__((format(printf, 2, 3))) int fail(int code, const char* fmt, ...)
 enum SlotState : int { kFree = 0, kQueued = 1, kDone = 2, kCollected = 3 };
 
 struct Slot {
-    uint16_t* q = nullptr;     // pinned [max_requests][Hq][d]
-    uint16_t* kn = nullptr;    // pinned [max_requests][Hkv][d]
+    uint16_t* q = nullptr;     // pinned: [B][Hq][d] q, then [B][Hkv][d] kn and vn
+    uint16_t* kn = nullptr;    // inside the q allocation, placed per submit
     uint16_t* vn = nullptr;
     uint16_t* out = nullptr;   // pinned [max_requests][Hq][d]
     hipEvent_t in_done = nullptr;
@@ -160,8 +160,6 @@ void free_all(apex_overlap* rt)
 {
     for (Slot& s : rt->slots) {
         if (s.q) (void)hipHostFree(s.q);
-        if (s.kn) (void)hipHostFree(s.kn);
-        if (s.vn) (void)hipHostFree(s.vn);
         if (s.out) (void)hipHostFree(s.out);
         if (s.in_done) (void)hipEventDestroy(s.in_done);
         if (s.out_done) (void)hipEventDestroy(s.out_done);
@@ -254,9 +252,10 @@ int apex_overlap_create(const apex_overlap_config* cfg, apex_overlap** out)
     for (size_t i = 0; i < rt->slots.size() && rc == APEX_OK; ++i) {
         Slot& s = rt->slots[i];
         s.layer = (int)(i / rt->per_layer);
-        if ((rc = host_alloc((void**)&s.q, rt->q_bytes(c.max_requests))) != APEX_OK) break;
-        if ((rc = host_alloc((void**)&s.kn, rt->kv_bytes(c.max_requests))) != APEX_OK) break;
-        if ((rc = host_alloc((void**)&s.vn, rt->kv_bytes(c.max_requests))) != APEX_OK) break;
+        // q, kn, vn share one allocation; submit() places kn and vn right
+        // after the B rows of q so that packed device rows copy in one go
+        if ((rc = host_alloc((void**)&s.q, rt->q_bytes(c.max_requests) + 2 * rt->kv_bytes(c.max_requests))) != APEX_OK)
+            break;
         if ((rc = host_alloc((void**)&s.out, rt->q_bytes(c.max_requests))) != APEX_OK) break;
         // the compute thread sleeps on in_done instead of spinning a core
         e = hipEventCreateWithFlags(&s.in_done, hipEventDisableTiming | hipEventBlockingSync);
@@ -340,9 +339,19 @@ int apex_overlap_submit(apex_overlap* rt, int layer, const void* q, const void* 
     }
     s.stride = stride;
     s.B = B;
-    hipError_t e = hipMemcpyAsync(s.q, q, rt->q_bytes(B), hipMemcpyDeviceToHost, st_);
-    if (e == hipSuccess) e = hipMemcpyAsync(s.kn, k_new, rt->kv_bytes(B), hipMemcpyDeviceToHost, st_);
-    if (e == hipSuccess) e = hipMemcpyAsync(s.vn, v_new, rt->kv_bytes(B), hipMemcpyDeviceToHost, st_);
+    s.kn = s.q + rt->q_bytes(B) / 2;
+    s.vn = s.kn + rt->kv_bytes(B) / 2;
+    hipError_t e;
+    if ((const char*)k_new == (const char*)q + rt->q_bytes(B) &&
+        (const char*)v_new == (const char*)k_new + rt->kv_bytes(B)) {
+        // q, k_new and v_new back to back on the device: one copy into the
+        // (equally back-to-back) staging buffers
+        e = hipMemcpyAsync(s.q, q, rt->q_bytes(B) + 2 * rt->kv_bytes(B), hipMemcpyDeviceToHost, st_);
+    } else {
+        e = hipMemcpyAsync(s.q, q, rt->q_bytes(B), hipMemcpyDeviceToHost, st_);
+        if (e == hipSuccess) e = hipMemcpyAsync(s.kn, k_new, rt->kv_bytes(B), hipMemcpyDeviceToHost, st_);
+        if (e == hipSuccess) e = hipMemcpyAsync(s.vn, v_new, rt->kv_bytes(B), hipMemcpyDeviceToHost, st_);
+    }
     if (e == hipSuccess) e = hipEventRecord(s.in_done, st_);
     if (e != hipSuccess) return fail(APEX_ERR_HIP, "copy of the new rows to the host failed: %s", hipGetErrorString(e));
     s.ticket = (seq << 16) | layer;

@@ -51,8 +51,9 @@ class Requests:
     table and lengths, and the next token's rows (host copies for the oracle,
     device copies for the runtime)."""
 
-    def __init__(self, torch, lens, num_blocks, seed):
+    def __init__(self, torch, lens, num_blocks, seed, packed=False):
         self.rng = np.random.default_rng(seed)
+        self.packed = packed
         self.layout = W.make_layout(lens, 16, self.rng, "random", slack_blocks=num_blocks - sum(
             -(-L // 16) for L in lens), stride=32)
         self.lens = self.layout.lens.copy()
@@ -78,6 +79,13 @@ class Requests:
         self.slots = W.append_slots(lay)
         dev = "cuda"
         t = self.torch
+        if self.packed:
+            # q | k | v back to back in one device buffer (one copy to the host)
+            flat = np.concatenate([self.q.ravel(), self.kn.ravel(), self.vn.ravel()])
+            d = t.from_numpy(flat).to(dev)
+            nq, nk = self.q.size, self.kn.size
+            return (d[:nq].view(self.q.shape), d[nq:nq + nk].view(self.kn.shape),
+                    d[nq + nk:].view(self.vn.shape))
         return (t.from_numpy(self.q).to(dev), t.from_numpy(self.kn).to(dev),
                 t.from_numpy(self.vn).to(dev))
 
@@ -96,10 +104,11 @@ def assert_close(got, ref, what):
     assert err <= MAX_ABS and rel <= REL_L2, what
 
 
-def test_single_submit_matches_oracles(torch_cuda, ov, oracle_mod):
+@pytest.mark.parametrize("packed", [False, True])
+def test_single_submit_matches_oracles(torch_cuda, ov, oracle_mod, packed):
     torch = torch_cuda
     with make_runtime(ov) as rt:
-        req = Requests(torch, [17, 64, 200, 1, 100, 15], 96, seed=1)
+        req = Requests(torch, [17, 64, 200, 1, 100, 15], 96, seed=1, packed=packed)
         k, v = rt.host_cache(0)
         req.fill(k, v)
         kb, vb = k.copy(), v.copy()
@@ -120,7 +129,7 @@ def test_deferred_collection_over_iterations(torch_cuda, ov, oracle_mod):
     torch = torch_cuda
     layers = 3
     with make_runtime(ov, layers=layers) as rt:
-        reqs = [Requests(torch, [30, 47, 5, 120], 96, seed=10 + l) for l in range(layers)]
+        reqs = [Requests(torch, [30, 47, 5, 120], 96, seed=10 + l, packed=l % 2 == 1) for l in range(layers)]
         for l in range(layers):
             reqs[l].fill(*rt.host_cache(l))
         prev = None
