@@ -99,7 +99,8 @@ typedef struct apex_decode_args {
     /* work groups of the persistent launch; 0 = as many as the device keeps
      * resident.  The work (one unit = one 16-token block of one kv-head) is
      * cut into equal contiguous ranges, one per work group; with 0 a range is
-     * never shorter than 8 units, with n > 0 every range holds at least one
+     * never shorter than 8 units unless that would leave fewer ranges than
+     * non-empty (request, kv-head) pairs, with n > 0 every range holds at least one
      * unit (tests use this to force split requests) */
     int num_workers;
     /* caller-owned device workspace of at least apex_decode_workspace_bytes()

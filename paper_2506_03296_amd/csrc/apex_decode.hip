@@ -217,11 +217,14 @@ int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block
     if (B > 0 && !context_lens) return fail(APEX_ERR_INVALID_ARG, "context_lens is NULL");
     if (block_size != apex::kBlockSize)
         return fail(APEX_ERR_UNSUPPORTED, "block_size %d unsupported (only 16)", block_size);
-    int64_t blocks = 0;
-    for (int b = 0; b < B; ++b) blocks += apex::blocks_of(context_lens[b], block_size);
+    int64_t blocks = 0, nonempty = 0;
+    for (int b = 0; b < B; ++b) {
+        blocks += apex::blocks_of(context_lens[b], block_size);
+        nonempty += context_lens[b] > 0;
+    }
     const int64_t units = blocks * Hkv;
     const int64_t W = apex::active_workers(units, launched_workers,
-                                           forced ? 1 : apex::kMinUnitsPerWorker);
+                                           forced ? 1 : apex::kMinUnitsPerWorker, nonempty * Hkv);
     int64_t partials = 0, pre = 0;
     for (int b = 0; b < B; ++b) {
         const int64_t nb = apex::blocks_of(context_lens[b], block_size);

@@ -330,6 +330,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     __shared__ int s_lens[kCachedLens];
     __shared__ int s_wsum[kWaves];
     __shared__ int s_wmax[kWaves];
+    __shared__ int s_wcnt[kWaves];
     __shared__ int s_loc_b;
     __shared__ int64_t s_loc_pre;
     __shared__ int s_last;
@@ -344,17 +345,18 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     // 1. partition.  context_lens is read from memory once: each thread sums
     // the blocks of a contiguous run of requests (and keeps the lengths in
     // LDS when they fit); wave-level scans plus one barrier give the prefix
-    // sums, the total and the longest request.
+    // sums, the total, the longest request and the non-empty requests.
     const int seg = (B + kAttnThreads - 1) / kAttnThreads;
     const int r0 = min(B, tid * seg);
     const int r1 = min(B, r0 + seg);
-    int tsum = 0, tmax = 0;
+    int tsum = 0, tmax = 0, tcnt = 0;
     for (int b = r0; b < r1; ++b) {
         const int L = lens[b];
         if (cached) s_lens[b] = L;
         const int nb = (int)blocks_of(L, kBlockSize);
         tsum += nb;
         tmax = max(tmax, nb);
+        tcnt += nb > 0;
     }
     int incl = tsum;
 #pragma unroll
@@ -363,22 +365,30 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         if (lane >= d) incl += y;
     }
 #pragma unroll
-    for (int d = 1; d < 64; d <<= 1) tmax = max(tmax, __shfl_xor(tmax, d, 64));
+    for (int d = 1; d < 64; d <<= 1) {
+        tmax = max(tmax, __shfl_xor(tmax, d, 64));
+        tcnt += __shfl_xor(tcnt, d, 64);
+    }
     if (lane == 63) s_wsum[wave] = incl;
-    if (lane == 0) s_wmax[wave] = tmax;
+    if (lane == 0) {
+        s_wmax[wave] = tmax;
+        s_wcnt[wave] = tcnt;
+    }
     __syncthreads();
-    int total = 0, maxb = 0;
+    int total = 0, maxb = 0, nonempty = 0;
 #pragma unroll
     for (int v = 0; v < kWaves; ++v) {
         if (v < wave) incl += s_wsum[v];
         total += s_wsum[v];
         maxb = max(maxb, s_wmax[v]);
+        nonempty += s_wcnt[v];
     }
     auto len_of = [&](int b) -> int { return cached ? s_lens[b] : lens[b]; };
 
     const int64_t units = (int64_t)uniform(total) * p.Hkv;
     const int64_t stride = p.bt_stride > 0 ? p.bt_stride : (int64_t)uniform(maxb);
-    const int64_t W = active_workers(units, (int64_t)gridDim.x, p.min_units);
+    const int64_t W = active_workers(units, (int64_t)gridDim.x, p.min_units,
+                                     (int64_t)uniform(nonempty) * p.Hkv);
     const int64_t u0 = units > 0 && w < W ? worker_start(w, units, W) : 0;
     const int64_t u1 = units > 0 && w < W ? worker_start(w + 1, units, W) : 0;
 

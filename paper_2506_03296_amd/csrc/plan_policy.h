@@ -30,11 +30,15 @@ __host__ __device__ inline int64_t blocks_of(int32_t len, int bs)
     return len > 0 ? ((int64_t)len + bs - 1) / bs : 0;
 }
 
-// Workers that get units: at most the launched ones, and none with fewer than
-// min_units units on average.
-__host__ __device__ inline int64_t active_workers(int64_t units, int64_t launched, int min_units)
+// Workers that get units: at most the launched ones; enough that each has
+// about min_units units, but never fewer than the non-empty (request,
+// kv-head) pairs -- a small batch would otherwise queue several short pairs
+// on one work group, one after another, while most of the device idles.
+__host__ __device__ inline int64_t active_workers(int64_t units, int64_t launched, int min_units,
+                                                  int64_t pairs)
 {
     int64_t w = units / (min_units > 0 ? min_units : 1);
+    if (w < pairs) w = pairs;
     if (w < 1) w = 1;
     return w < launched ? w : launched;
 }

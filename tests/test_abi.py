@@ -73,7 +73,8 @@ def test_args_struct_matches_header_field_order():
 def _brute_partition(lens, Hkv, launched, forced):
     blocks = [(-(-int(L) // 16)) if L > 0 else 0 for L in lens]
     U = sum(blocks) * Hkv
-    W = min(launched, max(1, U // (1 if forced else 8)))
+    pairs = sum(1 for nb in blocks if nb > 0) * Hkv
+    W = min(launched, max(1, U // (1 if forced else 8), pairs))
     owner = []
     starts = [w * U // W for w in range(W + 1)]
     for w in range(W):
