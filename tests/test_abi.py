@@ -116,6 +116,14 @@ def test_partition_random_batches(lib, seed):
     _check_plan(lens, Hkv, int(rng.choice([1, 3, 64, 100000])), forced=True)
 
 
+def test_partition_past_the_cached_lengths(lib):
+    rng = np.random.default_rng(9)
+    for B in (2048, 2049, 5000):
+        lens = rng.integers(0, 48, size=B)
+        _check_plan(lens, 2, 768)
+        _check_plan(lens, 2, 3, forced=True)
+
+
 def test_partition_edge_lengths(lib):
     for L in (0, 1, 15, 16, 17, 31, 32, 33, 16 * 8, 16 * 8 + 1, 32768):
         _check_plan([L], 8, 1024)

@@ -253,3 +253,37 @@ def test_full_size_sampled_parity(torch_cuda, apex, oracle_mod, name):
     assert_parity(got, ref, f"{name} requests {picks}")
     del wl
     torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------------------
+# batches past the lengths the kernel keeps in LDS (2048 requests), and one
+# request split over ~100 work groups (combine in several chunks of 8)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("B", [2048, 2049, 5000])
+def test_large_batches_read_lengths_from_memory(torch_cuda, apex, oracle_mod, B):
+    rng = np.random.default_rng(B)
+    lens = rng.integers(0, 48, size=B)
+    lens[rng.random(B) < 0.2] = 0
+    case = W.make_host_case(lens, 8, 2, seed=B, poison=True)
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale)
+    for workers in (0, 3):
+        got = run_gpu(torch_cuda, apex, case, num_workers=workers)
+        assert_parity(got, ref, f"B={B} workers={workers}")
+        assert np.all(got[lens == 0] == 0)
+
+
+def test_one_long_request_split_over_many_work_groups(torch_cuda, apex, oracle_mod):
+    torch = torch_cuda
+    case = W.make_host_case([65536], 32, 8, seed=65, poison=True)
+    ref, lse_ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache,
+                                                   case.block_table, case.context_lens, case.scale,
+                                                   return_lse=True)
+    plan = apex.plan_host(case.context_lens, 8, 768)
+    print(f"[parity] contributors per pair: {plan['contributors'].ravel().tolist()}", flush=True)
+    assert plan["contributors"].min() > 8          # more than one combine chunk
+    lse = torch.empty((1, 32), dtype=torch.float32, device="cuda")
+    got = run_gpu(torch, apex, case, num_workers=768, lse_out=lse)
+    assert_parity(got, ref, "L=65536")
+    assert np.max(np.abs(lse.cpu().numpy() - lse_ref)) < 1e-4
