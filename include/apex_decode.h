@@ -100,8 +100,10 @@ typedef struct apex_decode_args {
      * resident.  The work (one unit = one 16-token block of one kv-head) is
      * cut into equal contiguous ranges, one per work group; with 0 a range is
      * never shorter than 8 units unless that would leave fewer ranges than
-     * non-empty (request, kv-head) pairs, with n > 0 every range holds at least one
-     * unit (tests use this to force split requests) */
+     * non-empty (request, kv-head) pairs, and a batch of at most one pair per
+     * CU (and at most 1024 units per CU) uses one work group per CU; with
+     * n > 0 every range holds at least one unit (tests use this to force
+     * split requests) */
     int num_workers;
     /* caller-owned device workspace of at least apex_decode_workspace_bytes()
      * bytes and 256-byte aligned, or NULL for the library-owned one.  Its
@@ -130,15 +132,17 @@ size_t apex_decode_counter_bytes(int B, int Hkv);
 /*
  * Host mirror of the work partition, for inspection and tests (no GPU
  * needed).  Inputs: host context_lens[B], Hkv, block_size, the number of
- * launched work groups, and whether that number was forced (num_workers > 0
- * in apex_decode_args).  Outputs (any may be NULL): contributors_out[B * Hkv]
- * = work groups that share each (request, kv-head) pair (1 = written
- * directly, more = combined from partials), *units_out = blocks x kv-heads,
- * *active_out = work groups that get units, *partials_out = partial results
- * written.
+ * launched work groups, whether that number was forced (num_workers > 0 in
+ * apex_decode_args), and the device's compute units (the default grid uses
+ * only one work group per CU for a batch of at most one (request, kv-head)
+ * pair per CU and at most 1024 units per CU; 0 leaves that rule out).
+ * Outputs (any may be NULL): contributors_out[B * Hkv] = work groups that
+ * share each (request, kv-head) pair (1 = written directly, more = combined
+ * from partials), *units_out = blocks x kv-heads, *active_out = work groups
+ * that get units, *partials_out = partial results written.
  */
 int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block_size,
-                          int launched_workers, int forced, int32_t* contributors_out,
+                          int launched_workers, int forced, int cus, int32_t* contributors_out,
                           int64_t* units_out, int64_t* active_out, int64_t* partials_out);
 
 /* Message for the last failed call on this thread ("" if none). */

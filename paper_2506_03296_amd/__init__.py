@@ -88,7 +88,7 @@ def load_library(path=None):
     lib.apex_decode_counter_bytes.restype = ctypes.c_size_t
     lib.apex_decode_counter_bytes.argtypes = [i32, i32]
     lib.apex_decode_plan_host.restype = i32
-    lib.apex_decode_plan_host.argtypes = [vp, i32, i32, i32, i32, i32, vp,
+    lib.apex_decode_plan_host.argtypes = [vp, i32, i32, i32, i32, i32, i32, vp,
                                           ctypes.POINTER(i64), ctypes.POINTER(i64),
                                           ctypes.POINTER(i64)]
     lib.apex_decode_last_error.restype = ctypes.c_char_p
@@ -214,10 +214,11 @@ def counter_bytes(B, Hkv):
     return int(load_library().apex_decode_counter_bytes(B, Hkv))
 
 
-def plan_host(context_lens, Hkv, launched_workers, block_size=16, forced=False):
-    """Host mirror of the work partition (no GPU).  Returns a dict with
-    'contributors' (numpy int32 [B][Hkv]: work groups sharing each pair) and
-    the scalars 'units', 'active' and 'partials'."""
+def plan_host(context_lens, Hkv, launched_workers, block_size=16, forced=False, cus=0):
+    """Host mirror of the work partition (no GPU).  ``cus`` = the device's
+    compute units for the one-group-per-CU rule of the default grid (0 = off).
+    Returns a dict with 'contributors' (numpy int32 [B][Hkv]: work groups
+    sharing each pair) and the scalars 'units', 'active' and 'partials'."""
     import numpy as np
     lens = np.ascontiguousarray(np.asarray(context_lens), dtype=np.int32)
     B = lens.shape[0]
@@ -225,7 +226,7 @@ def plan_host(context_lens, Hkv, launched_workers, block_size=16, forced=False):
     units, active, partials = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
     rc = load_library().apex_decode_plan_host(
         lens.ctypes.data if B else None, B, Hkv, block_size, launched_workers, int(bool(forced)),
-        contrib.ctypes.data, ctypes.byref(units), ctypes.byref(active), ctypes.byref(partials))
+        int(cus), contrib.ctypes.data, ctypes.byref(units), ctypes.byref(active), ctypes.byref(partials))
     _check(rc)
     return {"contributors": contrib[:B * Hkv].reshape(B, Hkv), "units": units.value,
             "active": active.value, "partials": partials.value}

@@ -89,8 +89,9 @@ int resident_groups(int G, int* out)
     return APEX_OK;
 }
 
-// Default persistent grid for group size G on device dev: CUs x resident groups.
-int default_workers(int dev, int G, int64_t* out)
+// Default persistent grid for group size G on device dev: CUs x resident
+// groups (and the CU count, if cus is not NULL).
+int default_workers(int dev, int G, int64_t* out, int* cus = nullptr)
 {
     if (dev < 0 || dev >= kMaxDevices) return fail(APEX_ERR_HIP, "device ordinal %d out of range", dev);
     std::lock_guard<std::mutex> lock(g_mutex);
@@ -108,6 +109,7 @@ int default_workers(int dev, int G, int64_t* out)
         if (rc != APEX_OK) return rc;
     }
     *out = (int64_t)s.num_cu * s.resident[gi];
+    if (cus) *cus = s.num_cu;
     return APEX_OK;
 }
 
@@ -208,11 +210,11 @@ size_t apex_decode_workspace_bytes(int B, int Hq, int Hkv, int d, int block_size
 }
 
 int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block_size,
-                          int launched_workers, int forced, int32_t* contributors_out,
+                          int launched_workers, int forced, int cus, int32_t* contributors_out,
                           int64_t* units_out, int64_t* active_out, int64_t* partials_out)
 {
     apex::clear_error();
-    if (B < 0 || Hkv <= 0 || launched_workers <= 0)
+    if (B < 0 || Hkv <= 0 || launched_workers <= 0 || cus < 0)
         return fail(APEX_ERR_INVALID_ARG, "bad partition arguments");
     if (B > 0 && !context_lens) return fail(APEX_ERR_INVALID_ARG, "context_lens is NULL");
     if (block_size != apex::kBlockSize)
@@ -224,7 +226,8 @@ int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block
     }
     const int64_t units = blocks * Hkv;
     const int64_t W = apex::active_workers(units, launched_workers,
-                                           forced ? 1 : apex::kMinUnitsPerWorker, nonempty * Hkv);
+                                           forced ? 1 : apex::kMinUnitsPerWorker, nonempty * Hkv,
+                                           forced ? 0 : cus);
     int64_t partials = 0, pre = 0;
     for (int b = 0; b < B; ++b) {
         const int64_t nb = apex::blocks_of(context_lens[b], block_size);
@@ -276,8 +279,9 @@ int apex_decode_attention_ex(const apex_decode_args* args)
     if (e != hipSuccess) return fail(APEX_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
     const int G = a.Hq / a.Hkv;
     int64_t workers = a.num_workers;
+    int cus = 0;   // the one-group-per-CU rule applies to the default grid only
     if (workers == 0) {
-        rc = default_workers(dev, G, &workers);
+        rc = default_workers(dev, G, &workers, &cus);
         if (rc != APEX_OK) return rc;
     }
 
@@ -319,6 +323,7 @@ int apex_decode_attention_ex(const apex_decode_args* args)
     p.Hq = a.Hq;
     p.Hkv = a.Hkv;
     p.min_units = a.num_workers > 0 ? 1 : apex::kMinUnitsPerWorker;
+    p.cus = cus;
 
     hipStream_t stream = (hipStream_t)a.stream;
     switch (G) {

@@ -58,6 +58,7 @@ struct AttnParams {
     int Hq;
     int Hkv;
     int min_units;         // minimum units per active worker
+    int cus;               // compute units for the one-group-per-CU rule (0 = off)
 };
 
 // Reinterpret one 32-bit word as two fp16 values.  Taken by value on purpose:
@@ -388,7 +389,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     const int64_t units = (int64_t)uniform(total) * p.Hkv;
     const int64_t stride = p.bt_stride > 0 ? p.bt_stride : (int64_t)uniform(maxb);
     const int64_t W = active_workers(units, (int64_t)gridDim.x, p.min_units,
-                                     (int64_t)uniform(nonempty) * p.Hkv);
+                                     (int64_t)uniform(nonempty) * p.Hkv, p.cus);
     const int64_t u0 = units > 0 && w < W ? worker_start(w, units, W) : 0;
     const int64_t u1 = units > 0 && w < W ? worker_start(w + 1, units, W) : 0;
 

@@ -24,6 +24,7 @@ namespace apex {
 constexpr int kHeadDim = 128;
 constexpr int kBlockSize = 16;
 constexpr int kMinUnitsPerWorker = 8;   // two blocks per wave of a 4-wave work group
+constexpr int64_t kUnitsPerCuForOne = 1024;   // 8 MiB of K/V per CU
 
 __host__ __device__ inline int64_t blocks_of(int32_t len, int bs)
 {
@@ -34,9 +35,15 @@ __host__ __device__ inline int64_t blocks_of(int32_t len, int bs)
 // about min_units units, but never fewer than the non-empty (request,
 // kv-head) pairs -- a small batch would otherwise queue several short pairs
 // on one work group, one after another, while most of the device idles.
+// With cus > 0 (the device's compute units), a batch of at most one pair per
+// CU and at most kUnitsPerCuForOne units per CU uses only the first `cus`
+// work groups: one per CU (work groups are handed out round-robin over the
+// XCDs and then over their CUs), no pair split between two groups, and no
+// second group sharing the CU.
 __host__ __device__ inline int64_t active_workers(int64_t units, int64_t launched, int min_units,
-                                                  int64_t pairs)
+                                                  int64_t pairs, int64_t cus)
 {
+    if (cus > 0 && pairs <= cus && units <= cus * kUnitsPerCuForOne && launched > cus) launched = cus;
     int64_t w = units / (min_units > 0 ? min_units : 1);
     if (w < pairs) w = pairs;
     if (w < 1) w = 1;

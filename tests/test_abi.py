@@ -70,10 +70,12 @@ def test_args_struct_matches_header_field_order():
 # work partition (host mirror) against a brute-force assignment of units
 # ---------------------------------------------------------------------------
 
-def _brute_partition(lens, Hkv, launched, forced):
+def _brute_partition(lens, Hkv, launched, forced, cus=0):
     blocks = [(-(-int(L) // 16)) if L > 0 else 0 for L in lens]
     U = sum(blocks) * Hkv
     pairs = sum(1 for nb in blocks if nb > 0) * Hkv
+    if not forced and cus > 0 and pairs <= cus and U <= 1024 * cus:
+        launched = min(launched, cus)
     W = min(launched, max(1, U // (1 if forced else 8), pairs))
     owner = []
     starts = [w * U // W for w in range(W + 1)]
@@ -94,9 +96,9 @@ def _brute_partition(lens, Hkv, launched, forced):
     return U, W, contrib, per_worker_partials
 
 
-def _check_plan(lens, Hkv, launched, forced=False):
-    p = A.plan_host(lens, Hkv, launched, forced=forced)
-    U, W, contrib, pwp = _brute_partition(lens, Hkv, launched, forced)
+def _check_plan(lens, Hkv, launched, forced=False, cus=0):
+    p = A.plan_host(lens, Hkv, launched, forced=forced, cus=cus)
+    U, W, contrib, pwp = _brute_partition(lens, Hkv, launched, forced, cus)
     assert p["units"] == U
     assert p["active"] == (W if U else 0)
     assert np.array_equal(p["contributors"], contrib)
@@ -114,6 +116,24 @@ def test_partition_random_batches(lib, seed):
     Hkv = int(rng.choice([1, 2, 8, 32]))
     _check_plan(lens, Hkv, int(rng.choice([1, 7, 80, 1024])))
     _check_plan(lens, Hkv, int(rng.choice([1, 3, 64, 100000])), forced=True)
+
+
+def test_partition_one_group_per_cu_rule(lib):
+    # at most one pair per CU and at most 1024 units per CU: only `cus` groups
+    p = _check_plan([2048] * 32, 8, 512, cus=256)
+    assert p["active"] == 256 and p["partials"] == 0          # one pair per group
+    p = _check_plan([16384] * 32, 8, 512, cus=256)            # 1024 units per CU: still
+    assert p["active"] == 256
+    p = _check_plan([16400] * 32, 8, 512, cus=256)            # one block more per pair: off
+    assert p["active"] == 512
+    p = _check_plan([4096] * 64, 8, 512, cus=256)             # two pairs per CU: off
+    assert p["active"] == 512
+    p = _check_plan([2048] * 32, 8, 512, forced=True, cus=256)   # forced grids: off
+    assert p["active"] == 512
+    rng = np.random.default_rng(4)
+    for _ in range(20):
+        B = int(rng.integers(1, 40))
+        _check_plan(rng.integers(0, 9000, size=B), int(rng.choice([1, 2, 8])), 512, cus=256)
 
 
 def test_partition_past_the_cached_lengths(lib):
@@ -216,6 +236,8 @@ def test_plan_host_rejects_bad_arguments(lib):
         A.plan_host([5], 8, 0)
     with pytest.raises(A.ApexError):
         A.plan_host([5], 8, 256, block_size=32)
+    with pytest.raises(A.ApexError):
+        A.plan_host([5], 8, 256, cus=-1)
 
 
 def test_counter_bytes(lib):
