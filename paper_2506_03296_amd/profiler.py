@@ -19,8 +19,9 @@ kv-heads of 128, MLP 14336), on the GPU it is run on and its host:
          attention (torch's scaled_dot_product_attention, causal, fp16) vs
          prompt tokens
 
-Times are seconds per layer: GPU ones from events around each call (median
-of the repetitions), CPU ones wall clock (best of the repetitions).  The
+Times are seconds per layer: GPU ones from events around each call with the
+calls queued back to back (median of the repetitions), CPU ones wall clock
+(best of the repetitions).  The
 output keys are those of apex_sched_profile.
 """
 import argparse
@@ -38,19 +39,22 @@ def _median(xs):
 
 
 def gpu_time(torch, fn, reps=20, warmup=3):
+    """Median seconds of fn's GPU work.  The stream is held by a spin kernel
+    while all repetitions are enqueued, so they run back to back as in an
+    engine's queued iteration and each event pair brackets the GPU work, not
+    the host's launch latency."""
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
-    ts = []
-    for _ in range(reps):
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(reps)]
+    torch.cuda._sleep(20_000_000)
+    for a, b in pairs:
         a.record()
         fn()
         b.record()
-        b.synchronize()
-        ts.append(a.elapsed_time(b) * 1e-3)
-    return _median(ts)
+    torch.cuda.synchronize()
+    return _median([a.elapsed_time(b) * 1e-3 for a, b in pairs])
 
 
 def decode_batch(torch, B, L, seed):
