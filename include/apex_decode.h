@@ -41,7 +41,8 @@
  *
  * Errors: every entry point returns an apex_status; on failure nothing has
  * been enqueued and apex_decode_last_error() returns a message
- * (thread-local).  Block ids out of range are not checked on the device.
+ * (thread-local).  Block ids out of range are not checked on the device
+ * unless apex_decode_attention_ex is asked to (APEX_DECODE_FLAG_CHECK_INPUTS).
  *
  * Work partition: one persistent kernel launch per call.  Each work group
  * derives the partition from context_lens itself, takes an equal share of
@@ -117,8 +118,22 @@ typedef struct apex_decode_args {
     /* optional pair of hipEvent_t recorded on `stream` immediately before and
      * after the attention kernel (for per-kernel timing); NULL = none */
     void* attn_kernel_events[2];
-    uint32_t flags; /* reserved, must be 0 */
+    /* APEX_DECODE_FLAG_* bits; other bits must be 0 */
+    uint32_t flags;
+    /* physical blocks in k_cache/v_cache; needed by APEX_DECODE_FLAG_CHECK_INPUTS */
+    int64_t num_blocks;
 } apex_decode_args;
+
+/*
+ * Input check (for debugging engines; a separate kernel build, the default
+ * path is unchanged): block ids outside [0, num_blocks) are never read --
+ * their blocks are skipped as if absent -- and a context longer than an
+ * explicit block_table_stride row is cut to the row.  Each case sets a bit
+ * of a per-device error word that apex_decode_check_device_error() returns.
+ */
+#define APEX_DECODE_FLAG_CHECK_INPUTS 1u
+#define APEX_DEVICE_ERR_BLOCK_ID 1u    /* a block id outside [0, num_blocks) */
+#define APEX_DEVICE_ERR_TABLE_ROW 2u   /* a context past its block-table row */
 
 int apex_decode_attention_ex(const apex_decode_args* args);
 
@@ -144,6 +159,10 @@ size_t apex_decode_counter_bytes(int B, int Hkv);
 int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block_size,
                           int launched_workers, int forced, int cus, int32_t* contributors_out,
                           int64_t* units_out, int64_t* active_out, int64_t* partials_out);
+
+/* Waits for the current device, returns the input-check error bits that
+ * checked calls on it set since the last read (0 if none), and clears them. */
+int apex_decode_check_device_error(uint32_t* error_bits);
 
 /* Message for the last failed call on this thread ("" if none). */
 const char* apex_decode_last_error(void);

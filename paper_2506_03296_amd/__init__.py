@@ -19,7 +19,8 @@ __all__ = [
     "ApexError", "LIB_PATH", "load_library", "decode_attention", "decode_attention_ex",
     "workspace_bytes", "plan_host", "last_error", "release_workspace", "version",
     "APEX_OK", "APEX_ERR_INVALID_ARG", "APEX_ERR_UNSUPPORTED", "APEX_ERR_OUT_OF_MEMORY",
-    "APEX_ERR_HIP", "EXPORTED_SYMBOLS", "counter_bytes", "kv_append",
+    "APEX_ERR_HIP", "EXPORTED_SYMBOLS", "counter_bytes", "kv_append", "check_device_error",
+    "FLAG_CHECK_INPUTS", "DEVICE_ERR_BLOCK_ID", "DEVICE_ERR_TABLE_ROW",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libapex_decode.so")
@@ -34,7 +35,11 @@ EXPORTED_SYMBOLS = (
     "apex_decode_attention", "apex_decode_attention_ex", "apex_decode_workspace_bytes",
     "apex_decode_counter_bytes", "apex_decode_plan_host", "apex_decode_last_error",
     "apex_decode_release_workspace", "apex_decode_version", "apex_kv_append",
+    "apex_decode_check_device_error",
 )
+FLAG_CHECK_INPUTS = 1
+DEVICE_ERR_BLOCK_ID = 1
+DEVICE_ERR_TABLE_ROW = 2
 
 
 class ApexError(RuntimeError):
@@ -55,6 +60,7 @@ class DecodeArgs(ctypes.Structure):
         ("workspace", ctypes.c_void_p),
         ("workspace_bytes", ctypes.c_size_t), ("lse_out", ctypes.c_void_p),
         ("attn_kernel_events", ctypes.c_void_p * 2), ("flags", ctypes.c_uint32),
+        ("num_blocks", ctypes.c_int64),
     ]
 
 
@@ -97,6 +103,8 @@ def load_library(path=None):
     lib.apex_decode_release_workspace.argtypes = []
     lib.apex_decode_version.restype = i32
     lib.apex_decode_version.argtypes = []
+    lib.apex_decode_check_device_error.restype = i32
+    lib.apex_decode_check_device_error.argtypes = [ctypes.POINTER(ctypes.c_uint32)]
     lib.apex_kv_append.restype = i32
     lib.apex_kv_append.argtypes = [vp, vp, i64, vp, vp, vp, i32, i32, i32, i32, i64, vp]
     if path is None:
@@ -175,13 +183,14 @@ def decode_attention(q, k_cache, v_cache, block_table, context_lens, scale, out=
 
 def decode_attention_ex(q, k_cache, v_cache, block_table, context_lens, scale, out=None,
                         block_table_stride=0, num_workers=0, workspace=None,
-                        lse_out=None, events=None, stream=None):
+                        lse_out=None, events=None, stream=None, check_inputs=False):
     """apex_decode_attention_ex over torch tensors; returns ``out``.
 
     ``workspace`` is an optional uint8 device tensor (caller-owned; its first
     counter_bytes(B, Hkv) bytes must be zero, e.g. from torch.zeros);
     ``events`` an optional pair of torch.cuda.Event recorded around the
-    attention kernel."""
+    attention kernel; ``check_inputs`` runs the input-checking kernel (block
+    ids against the caches' block count; see check_device_error)."""
     import torch
     B, Hq, Hkv, d, bs = _shapes(q, k_cache)
     if out is None:
@@ -202,8 +211,19 @@ def decode_attention_ex(q, k_cache, v_cache, block_table, context_lens, scale, o
     if events is not None:
         a.attn_kernel_events[0] = _event_handle(events[0], s)
         a.attn_kernel_events[1] = _event_handle(events[1], s)
+    if check_inputs:
+        a.flags = FLAG_CHECK_INPUTS
+        a.num_blocks = k_cache.shape[0]
     _check(load_library().apex_decode_attention_ex(ctypes.byref(a)))
     return out
+
+
+def check_device_error():
+    """Waits for the current device and returns (and clears) the error bits
+    set by input-checking calls (DEVICE_ERR_*; 0 = none)."""
+    bits = ctypes.c_uint32()
+    _check(load_library().apex_decode_check_device_error(ctypes.byref(bits)))
+    return bits.value
 
 
 def workspace_bytes(B, Hq, Hkv, d=128, block_size=16, num_workers=0):

@@ -56,6 +56,7 @@ struct DeviceState {
     int resident[kGroupKinds] = {0, 0, 0, 0};   // work groups per CU, per G
     Buffer counters;   // zeroed at allocation; calls leave it zero
     Buffer partials;
+    Buffer error_word;   // input-check error bits, zeroed at allocation and when read
 };
 
 std::mutex g_mutex;
@@ -78,10 +79,10 @@ int resident_groups(int G, int* out)
     int n = 0;
     hipError_t e;
     switch (G) {
-        case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<1>, apex::kAttnThreads, 0); break;
-        case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<2>, apex::kAttnThreads, 0); break;
-        case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<4>, apex::kAttnThreads, 0); break;
-        default: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<8>, apex::kAttnThreads, 0); break;
+        case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<1, false>, apex::kAttnThreads, 0); break;
+        case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<2, false>, apex::kAttnThreads, 0); break;
+        case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<4, false>, apex::kAttnThreads, 0); break;
+        default: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<8, false>, apex::kAttnThreads, 0); break;
     }
     if (e != hipSuccess || n <= 0)
         return fail(APEX_ERR_HIP, "occupancy query failed: %s", hipGetErrorString(e));
@@ -165,7 +166,7 @@ int check_shapes(int B, int Hq, int Hkv, int d, int block_size)
     return APEX_OK;
 }
 
-template <int G>
+template <int G, bool kCheck>
 int launch(const apex::AttnParams& p, const int32_t* bt, const int32_t* lens, int64_t workers,
            void* const* events, hipStream_t stream)
 {
@@ -173,7 +174,7 @@ int launch(const apex::AttnParams& p, const int32_t* bt, const int32_t* lens, in
         hipError_t e = hipEventRecord((hipEvent_t)events[0], stream);
         if (e != hipSuccess) return fail(APEX_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
     }
-    apex::attn_kernel<G><<<(unsigned)workers, apex::kAttnThreads, 0, stream>>>(p, bt, lens);
+    apex::attn_kernel<G, kCheck><<<(unsigned)workers, apex::kAttnThreads, 0, stream>>>(p, bt, lens);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(APEX_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     if (events[1]) {
@@ -187,7 +188,7 @@ int launch(const apex::AttnParams& p, const int32_t* bt, const int32_t* lens, in
 
 extern "C" {
 
-int apex_decode_version(void) { return 200; }
+int apex_decode_version(void) { return 300; }
 
 const char* apex_decode_last_error(void) { return apex::last_error_message(); }
 
@@ -255,7 +256,10 @@ int apex_decode_attention_ex(const apex_decode_args* args)
     const apex_decode_args& a = *args;
     int rc = check_shapes(a.B, a.Hq, a.Hkv, a.d, a.block_size);
     if (rc != APEX_OK) return rc;
-    if (a.flags != 0) return fail(APEX_ERR_INVALID_ARG, "flags must be 0");
+    if (a.flags & ~APEX_DECODE_FLAG_CHECK_INPUTS) return fail(APEX_ERR_INVALID_ARG, "unknown flags");
+    const bool check = (a.flags & APEX_DECODE_FLAG_CHECK_INPUTS) != 0;
+    if (check && a.num_blocks <= 0)
+        return fail(APEX_ERR_INVALID_ARG, "the input check needs num_blocks > 0");
     if (a.num_workers < 0 || a.num_workers > kMaxWorkers)
         return fail(APEX_ERR_INVALID_ARG, "num_workers = %d out of range", a.num_workers);
     if (a.block_table_stride < 0) return fail(APEX_ERR_INVALID_ARG, "block_table_stride is negative");
@@ -306,6 +310,13 @@ int apex_decode_attention_ex(const apex_decode_args* args)
         counters = s.counters.ptr;
         partials = s.partials.ptr;
     }
+    void* error_word = nullptr;
+    if (check) {
+        std::lock_guard<std::mutex> lock(g_mutex);
+        rc = grow(g_dev[dev].error_word, 4, true);
+        if (rc != APEX_OK) return rc;
+        error_word = g_dev[dev].error_word.ptr;
+    }
 
     apex::AttnParams p;
     p.q = (const apex::f16*)a.q;
@@ -324,13 +335,26 @@ int apex_decode_attention_ex(const apex_decode_args* args)
     p.Hkv = a.Hkv;
     p.min_units = a.num_workers > 0 ? 1 : apex::kMinUnitsPerWorker;
     p.cus = cus;
+    p.num_blocks = check ? a.num_blocks : 0;
+    p.error_word = (unsigned*)error_word;
 
     hipStream_t stream = (hipStream_t)a.stream;
+    const int32_t* bt = a.block_table;
+    const int32_t* lens = a.context_lens;
+    void* const* ev = a.attn_kernel_events;
+    if (check) {
+        switch (G) {
+            case 1: return launch<1, true>(p, bt, lens, workers, ev, stream);
+            case 2: return launch<2, true>(p, bt, lens, workers, ev, stream);
+            case 4: return launch<4, true>(p, bt, lens, workers, ev, stream);
+            default: return launch<8, true>(p, bt, lens, workers, ev, stream);
+        }
+    }
     switch (G) {
-        case 1: return launch<1>(p, a.block_table, a.context_lens, workers, a.attn_kernel_events, stream);
-        case 2: return launch<2>(p, a.block_table, a.context_lens, workers, a.attn_kernel_events, stream);
-        case 4: return launch<4>(p, a.block_table, a.context_lens, workers, a.attn_kernel_events, stream);
-        default: return launch<8>(p, a.block_table, a.context_lens, workers, a.attn_kernel_events, stream);
+        case 1: return launch<1, false>(p, bt, lens, workers, ev, stream);
+        case 2: return launch<2, false>(p, bt, lens, workers, ev, stream);
+        case 4: return launch<4, false>(p, bt, lens, workers, ev, stream);
+        default: return launch<8, false>(p, bt, lens, workers, ev, stream);
     }
 }
 
@@ -356,6 +380,25 @@ int apex_decode_attention(const void* q, const void* k_cache, const void* v_cach
     return apex_decode_attention_ex(&a);
 }
 
+int apex_decode_check_device_error(uint32_t* error_bits)
+{
+    apex::clear_error();
+    if (!error_bits) return fail(APEX_ERR_INVALID_ARG, "error_bits is NULL");
+    *error_bits = 0;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(APEX_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices) return fail(APEX_ERR_HIP, "device ordinal %d out of range", dev);
+    std::lock_guard<std::mutex> lock(g_mutex);
+    Buffer& w = g_dev[dev].error_word;
+    if (!w.ptr) return APEX_OK;   // no checked call ran on this device
+    e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = hipMemcpy(error_bits, w.ptr, 4, hipMemcpyDeviceToHost);
+    if (e == hipSuccess) e = hipMemset(w.ptr, 0, 4);
+    if (e != hipSuccess) return fail(APEX_ERR_HIP, "reading the error word: %s", hipGetErrorString(e));
+    return APEX_OK;
+}
+
 int apex_decode_release_workspace(void)
 {
     apex::clear_error();
@@ -363,14 +406,16 @@ int apex_decode_release_workspace(void)
     int rc = APEX_OK;
     for (int d = 0; d < kMaxDevices; ++d) {
         DeviceState& s = g_dev[d];
-        if (!s.counters.ptr && !s.partials.ptr) continue;
+        if (!s.counters.ptr && !s.partials.ptr && !s.error_word.ptr) continue;
         int prev = 0;
         (void)hipGetDevice(&prev);
         if (hipSetDevice(d) == hipSuccess && hipDeviceSynchronize() == hipSuccess) {
             if (s.counters.ptr) (void)hipFree(s.counters.ptr);
             if (s.partials.ptr) (void)hipFree(s.partials.ptr);
+            if (s.error_word.ptr) (void)hipFree(s.error_word.ptr);
             s.counters = Buffer();
             s.partials = Buffer();
+            s.error_word = Buffer();
         } else {
             rc = fail(APEX_ERR_HIP, "could not release the workspaces of device %d", d);
         }

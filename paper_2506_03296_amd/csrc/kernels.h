@@ -59,7 +59,18 @@ struct AttnParams {
     int Hkv;
     int min_units;         // minimum units per active worker
     int cus;               // compute units for the one-group-per-CU rule (0 = off)
+    int64_t num_blocks;    // physical blocks in the caches (input check only)
+    unsigned* error_word;  // input-check error bits (input check only)
 };
+
+// Input-check error bits (apex_decode.h: APEX_DEVICE_ERR_*).
+constexpr unsigned kErrBlockId = 1u;      // a block id outside [0, num_blocks)
+constexpr unsigned kErrTableRow = 2u;     // a context past its block-table row
+
+__device__ inline void report_error(const AttnParams& p, unsigned bits)
+{
+    __hip_atomic_fetch_or(p.error_word, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // Reinterpret one 32-bit word as two fp16 values.  Taken by value on purpose:
 // clang's __builtin_bit_cast applied directly to a vector element expression
@@ -158,7 +169,7 @@ __device__ inline void load_slab(u32x4 (&w)[4], const f16* slab, int bytes, int 
 // h, log2 units, equal on the four lanes of h), l (sum of the weights of its
 // tokens) and acc[t][i] (running P.V of head h at dim 32q + 8i + t).  On
 // return the wave's state is in s_acc/s_m/s_l.
-template <int G>
+template <int G, bool kCheck>
 __device__ inline void wave_attend(const AttnParams& p, const int32_t* __restrict__ bt_row, int b,
                                    int g, int L, int lo, int hi, int wave, int lane,
                                    float (*s_acc)[G][kHeadDim], float (*s_m)[G], float (*s_l)[G])
@@ -202,12 +213,23 @@ __device__ inline void wave_attend(const AttnParams& p, const int32_t* __restric
     const int koff = k_lane_offset(lane);
     const int voff = v_lane_offset(lane);
     auto id_of = [&](int k) -> int { return k < n ? bt_w[kWaves * k] : 0; };
-    auto bytes_of = [&](int k) -> int { return k < n ? kSlabBytes : 0; };
+    // with the input check, a block id outside the pool is never read: its
+    // loads get a zero extent like those past the end
+    auto id_ok = [&](int id) -> bool { return !kCheck || (id >= 0 && (int64_t)id < p.num_blocks); };
+    auto bytes_of = [&](int k, int id) -> int { return k < n && id_ok(id) ? kSlabBytes : 0; };
 
-    // One block: consume (kt, vt), refill them with block k + 2 (id2).
-    auto block_step = [&](u32x4 (&kt)[4], u32x4 (&vt)[4], int k, int id2) {
-        const int nbytes = bytes_of(k + 2);
+    // One block: consume (kt, vt) holding block k (id cur), refill them with
+    // block k + 2 (id2).
+    auto block_step = [&](u32x4 (&kt)[4], u32x4 (&vt)[4], int k, int id2, int cur) {
+        const int nbytes = bytes_of(k + 2, id2);
         const int tok0 = (first + kWaves * k) * BS;
+        if (kCheck && !id_ok(cur)) {
+            // skip the block (its tokens take no part), keep the pipeline going
+            if (lane == 0) report_error(p, kErrBlockId);
+            load_slab(kt, kpair + (uint64_t)(uint32_t)id2 * step, nbytes, koff, 64);
+            load_slab(vt, vpair + (uint64_t)(uint32_t)id2 * step, nbytes, voff, 256);
+            return;
+        }
 
         // S^T = K Q^T: lane (h, q) gets the scores of tokens 4q..4q+3 of head h
         f32x4 s = {0.f, 0.f, 0.f, 0.f};
@@ -274,21 +296,21 @@ __device__ inline void wave_attend(const AttnParams& p, const int32_t* __restric
     };
 
     u32x4 kt0[4], vt0[4], kt1[4], vt1[4];
-    {
-        const int id0 = id_of(0), id1 = id_of(1);
-        load_slab(kt0, kpair + (uint64_t)(uint32_t)id0 * step, bytes_of(0), koff, 64);
-        load_slab(vt0, vpair + (uint64_t)(uint32_t)id0 * step, bytes_of(0), voff, 256);
-        load_slab(kt1, kpair + (uint64_t)(uint32_t)id1 * step, bytes_of(1), koff, 64);
-        load_slab(vt1, vpair + (uint64_t)(uint32_t)id1 * step, bytes_of(1), voff, 256);
-    }
+    int cur0 = id_of(0), cur1 = id_of(1);   // ids of the blocks in the two tiles
+    load_slab(kt0, kpair + (uint64_t)(uint32_t)cur0 * step, bytes_of(0, cur0), koff, 64);
+    load_slab(vt0, vpair + (uint64_t)(uint32_t)cur0 * step, bytes_of(0, cur0), voff, 256);
+    load_slab(kt1, kpair + (uint64_t)(uint32_t)cur1 * step, bytes_of(1, cur1), koff, 64);
+    load_slab(vt1, vpair + (uint64_t)(uint32_t)cur1 * step, bytes_of(1, cur1), voff, 256);
     int ida = id_of(2), idb = id_of(3);   // ids of the blocks two steps ahead
     for (int k = 0; k < n; k += 2) {
         const int ida_next = id_of(k + 4);
-        block_step(kt0, vt0, k, ida);
+        block_step(kt0, vt0, k, ida, cur0);
+        cur0 = ida;
         ida = ida_next;
         if (k + 1 >= n) break;
         const int idb_next = id_of(k + 5);
-        block_step(kt1, vt1, k + 1, idb);
+        block_step(kt1, vt1, k + 1, idb, cur1);
+        cur1 = idb;
         idb = idb_next;
     }
 
@@ -319,7 +341,7 @@ __device__ inline void write_row(const AttnParams& p, int b, int head, int dim, 
             den > 0.f ? (M + __log2f(den)) * 0.69314718055994531f : -INFINITY;
 }
 
-template <int G>
+template <int G, bool kCheck>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2))) void attn_kernel(AttnParams p,
                                                         const int32_t* __restrict__ bt,
                                                         const int32_t* __restrict__ lens)
@@ -350,9 +372,16 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     const int seg = (B + kAttnThreads - 1) / kAttnThreads;
     const int r0 = min(B, tid * seg);
     const int r1 = min(B, r0 + seg);
+    // with the input check, a context longer than an explicit table row is
+    // cut to the row (and reported)
+    const int64_t row_tokens = p.bt_stride * kBlockSize;
+    auto clamp_len = [&](int L) -> int {
+        return kCheck && p.bt_stride > 0 && L > row_tokens ? (int)row_tokens : L;
+    };
     int tsum = 0, tmax = 0, tcnt = 0;
     for (int b = r0; b < r1; ++b) {
-        const int L = lens[b];
+        const int L = clamp_len(lens[b]);
+        if (kCheck && L != lens[b]) report_error(p, kErrTableRow);
         if (cached) s_lens[b] = L;
         const int nb = (int)blocks_of(L, kBlockSize);
         tsum += nb;
@@ -384,7 +413,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         maxb = max(maxb, s_wmax[v]);
         nonempty += s_wcnt[v];
     }
-    auto len_of = [&](int b) -> int { return cached ? s_lens[b] : lens[b]; };
+    auto len_of = [&](int b) -> int { return cached ? s_lens[b] : clamp_len(lens[b]); };
 
     const int64_t units = (int64_t)uniform(total) * p.Hkv;
     const int64_t stride = p.bt_stride > 0 ? p.bt_stride : (int64_t)uniform(maxb);
@@ -426,7 +455,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         const int take = (int)min((int64_t)(nb - blk), u1 - u);
         const int lo = blk, hi = blk + take;
         const int32_t* bt_row = bt + (size_t)uniform(b) * (size_t)stride;
-        wave_attend<G>(p, bt_row, b, g, L, lo, hi, wave, lane, s_acc, s_m, s_l);
+        wave_attend<G, kCheck>(p, bt_row, b, g, L, lo, hi, wave, lane, s_acc, s_m, s_l);
         __syncthreads();
 
         // 3. merge the waves, emit rows or a partial

@@ -218,7 +218,7 @@ def test_empty_batch_is_a_noop(lib):
 
 
 def test_ex_rejects_flags_and_negative_fields(lib):
-    for field, value in (("flags", 1), ("num_workers", -1), ("num_workers", 1 << 21),
+    for field, value in (("flags", 2), ("flags", 1), ("num_workers", -1), ("num_workers", 1 << 21),
                          ("block_table_stride", -5)):
         a = A.DecodeArgs()
         a.q, a.k_cache, a.v_cache = FAKE, FAKE + (1 << 30), FAKE + (2 << 30)
@@ -227,6 +227,17 @@ def test_ex_rejects_flags_and_negative_fields(lib):
         setattr(a, field, value)
         assert lib.apex_decode_attention_ex(ctypes.byref(a)) == A.APEX_ERR_INVALID_ARG
     assert lib.apex_decode_attention_ex(None) == A.APEX_ERR_INVALID_ARG
+
+
+def test_ex_check_flag_needs_the_block_count(lib):
+    a = A.DecodeArgs()
+    a.q, a.k_cache, a.v_cache = FAKE, FAKE + (1 << 30), FAKE + (2 << 30)
+    a.block_table, a.context_lens, a.out = FAKE + (3 << 30), FAKE + (4 << 30), FAKE + (5 << 30)
+    a.B, a.Hq, a.Hkv, a.d, a.block_size, a.scale = 2, 32, 8, 128, 16, 0.1
+    a.flags = A.FLAG_CHECK_INPUTS
+    a.num_blocks = 0
+    assert lib.apex_decode_attention_ex(ctypes.byref(a)) == A.APEX_ERR_INVALID_ARG
+    assert "num_blocks" in A.last_error()
 
 
 def test_plan_host_rejects_bad_arguments(lib):

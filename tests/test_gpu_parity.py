@@ -287,3 +287,54 @@ def test_one_long_request_split_over_many_work_groups(torch_cuda, apex, oracle_m
     got = run_gpu(torch, apex, case, num_workers=768, lse_out=lse)
     assert_parity(got, ref, "L=65536")
     assert np.max(np.abs(lse.cpu().numpy() - lse_ref)) < 1e-4
+
+
+# ---------------------------------------------------------------------------
+# input check (APEX_DECODE_FLAG_CHECK_INPUTS)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name,lens,Hq,Hkv", SMALL[:4], ids=[s[0] for s in SMALL[:4]])
+def test_checked_path_matches_default_path_bitwise(torch_cuda, apex, name, lens, Hq, Hkv):
+    case = W.make_host_case(lens, Hq, Hkv, seed=len(lens) * 17 + Hq, poison=True)
+    for workers in (0, 5):
+        plain = run_gpu(torch_cuda, apex, case, num_workers=workers)
+        checked = run_gpu(torch_cuda, apex, case, num_workers=workers, check_inputs=True)
+        assert np.array_equal(plain.view(np.uint16), checked.view(np.uint16)), name
+    assert apex.check_device_error() == 0
+
+
+def test_checked_path_skips_block_ids_outside_the_pool(torch_cuda, apex, oracle_mod):
+    case = W.make_host_case([40, 300, 17, 33], 32, 8, seed=90, poison=True)
+    nb = case.k_cache.shape[0]
+    bt = case.block_table.copy()
+    bt[0, 1] = nb + 3            # a middle block: tokens 16..31 of request 0
+    bt[1, 18] = -1               # the last block of request 1 (tokens 288..299)
+    bt[3, 2] = 2 ** 31 - 1       # the last block of request 3 (token 32)
+    bad = W.HostCase(case.q, case.k_cache, case.v_cache, bt, case.context_lens, case.scale)
+    assert apex.check_device_error() == 0
+    for workers in (0, 7, 1000):
+        got = run_gpu(torch_cuda, apex, bad, num_workers=workers, check_inputs=True)
+        assert apex.check_device_error() == apex.DEVICE_ERR_BLOCK_ID
+        # expected: the same attention with the bad blocks' tokens absent
+        exp_bt = case.block_table.copy()
+        exp_lens = case.context_lens.copy()
+        exp_bt[0, 1] = case.block_table[0, 2]      # tokens 32..39 move up to 16..23
+        exp_lens[0] = 24
+        exp_lens[1] = 288
+        exp_lens[3] = 32
+        ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, exp_bt, exp_lens,
+                                              case.scale)
+        assert_parity(got, ref, f"bad ids skipped, workers={workers}")
+    assert apex.check_device_error() == 0            # reading cleared the word
+
+
+def test_checked_path_cuts_a_context_to_its_table_row(torch_cuda, apex, oracle_mod):
+    case = W.make_host_case([40, 64], 16, 4, seed=91, poison=True, stride=4)
+    lens = case.context_lens.copy()
+    lens[1] = 100                 # longer than the 4-block row
+    longer = W.HostCase(case.q, case.k_cache, case.v_cache, case.block_table, lens, case.scale)
+    got = run_gpu(torch_cuda, apex, longer, block_table_stride=4, check_inputs=True)
+    assert apex.check_device_error() == apex.DEVICE_ERR_TABLE_ROW
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale)
+    assert_parity(got, ref, "context cut to the row")
