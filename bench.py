@@ -25,11 +25,13 @@ JSON line:
              GPU, 16 extra requests attended on the host; iteration time
              GPU-only (without the extra requests; and with their rows in
              the linears but no attention for them, the floor of the
-             overlap), with the overlap (results collected one iteration
-             later by a readiness check that never blocks; a result not yet
-             ready is checked again in the next iteration and waited for
-             only if still missing then) and with a blocking wait in every
-             layer
+             overlap), with the overlap (results collected by a readiness
+             check that never blocks; a layer whose previous result is still
+             out gets no new host work that iteration, so the host-attended
+             requests advance at the host's pace and the GPU never waits for
+             them; their tokens are counted from the collected jobs) and with
+             a blocking wait in every layer; every iteration ends with a host
+             synchronisation, as sampling the next tokens requires
   kv_append  the paged KV append that precedes each step (apex_kv_append),
              timed alone with events around its kernel: the step's own append
              (one token per request at position L_b - 1 of the workload's
@@ -267,59 +269,69 @@ def measure_overlap(A, torch, wl, layers=8, b_cpu=16, l_cpu=512, iters=16, warmu
     t_cpu = min(_timed(lambda: cpu.decode_attention(qh, hk, hk, table, lens0, wl.scale))
                 for _ in range(5))
 
-    times, late, stalls = {}, {}, {}
+    times, jobs = {}, {}
     for mode in ("gpu_only", "gpu_only_unified", "async_overlap", "sync_wait"):
-        # three result slots per layer: one in flight, one collected late
+        # two result slots per layer: one in flight, one being collected
         rt = overlap.Overlap(layers, b_cpu, cfg.Hq, cfg.Hkv, cfg.d, cfg.block_size, wl.scale,
-                             num_blocks, stride, threads=threads, slots_per_layer=3)
+                             num_blocks, stride, threads=threads)
         lens = np.full(b_cpu, l_cpu - 1, np.int32)
         pending = [[] for _ in range(layers)]   # tickets not yet collected, oldest first
-        counts = {"late": 0, "stall": 0}
+        counts = {"done": 0, "skipped": 0}
+
+        def slots_for(lens_now):
+            pos = lens_now - 1
+            return table[np.arange(b_cpu), pos // cfg.block_size].astype(np.int64) * cfg.block_size \
+                + pos % cfg.block_size
 
         def iteration():
             nonlocal lens
             lens = lens + 1
-            pos = lens - 1
-            slots = table[np.arange(b_cpu), pos // cfg.block_size].astype(np.int64) * cfg.block_size \
-                + pos % cfg.block_size
+            slots = slots_for(lens)
             for l in range(layers):
                 if mode.startswith("gpu_only"):
                     (lin_gpu if mode == "gpu_only" else lin_all)()
                     attn()
                     continue
                 lin_all()
-                if mode == "async_overlap" and len(pending[l]) == 2:
-                    # a result already one iteration late: it must be in now
-                    counts["stall"] += 1
-                    rt.wait(pending[l].pop(0), outs[l])
-                t = rt.submit(l, q_c, kn, vn, slots, table, lens)
-                attn()
                 if mode == "sync_wait":
+                    t = rt.submit(l, q_c, kn, vn, slots, table, lens)
+                    attn()
                     rt.wait(t, outs[l])
+                    counts["done"] += 1
                     continue
-                # readiness check of earlier results, never blocking: a result
-                # that is not ready is checked again in the next iteration
+                # readiness check, never blocking: collect what the host has
+                # finished; a layer whose previous result is still out gets no
+                # new work this iteration (its requests wait), the GPU goes on
                 while pending[l] and rt.poll(pending[l][0], outs[l]):
                     pending[l].pop(0)
-                counts["late"] += len(pending[l])
-                pending[l].append(t)
+                    counts["done"] += 1
+                if not pending[l]:
+                    pending[l].append(rt.submit(l, q_c, kn, vn, slots, table, lens))
+                else:
+                    counts["skipped"] += 1
+                attn()
+            # the iteration ends by sampling the next tokens: the host waits
+            # for the GPU once per iteration, as a decode loop does
+            torch.cuda.synchronize()
 
         for _ in range(warmup):
             iteration()
         torch.cuda.synchronize()
-        counts["late"] = counts["stall"] = 0
+        counts["done"] = counts["skipped"] = 0
         t0 = time.perf_counter()
         for _ in range(iters):
             iteration()
         torch.cuda.synchronize()
         times[mode] = (time.perf_counter() - t0) / iters
-        late[mode], stalls[mode] = counts["late"], counts["stall"]
+        jobs[mode] = dict(counts)
         for l in range(layers):
             for t in pending[l]:
                 rt.wait(t, outs[l])
         torch.cuda.synchronize()
         rt.close()
-    tok = {"gpu_only": cfg.B, "gpu_only_unified": cfg.B, "async_overlap": cfg.B + b_cpu,
+    # host-attended requests finish a token per `layers` collected jobs
+    tok = {"gpu_only": cfg.B, "gpu_only_unified": cfg.B,
+           "async_overlap": cfg.B + b_cpu * jobs["async_overlap"]["done"] / (layers * iters),
            "sync_wait": cfg.B + b_cpu}
     return {
         "runtime": "apex_overlap", "layers": layers, "gpu_requests": cfg.B, "cpu_requests": b_cpu,
@@ -327,10 +339,8 @@ def measure_overlap(A, torch, wl, layers=8, b_cpu=16, l_cpu=512, iters=16, warmu
         "iteration_ms": {k: round(v * 1e3, 3) for k, v in times.items()},
         "tokens_per_s": {k: round(tok[k] / v, 1) for k, v in times.items()},
         "host_attention_ms_per_layer": round(t_cpu * 1e3, 3),
-        "late_results": late["async_overlap"], "stalls": stalls["async_overlap"],
+        "host_jobs_done_per_layer_iteration": round(jobs["async_overlap"]["done"] / (layers * iters), 3),
         "overlap_cost_ms": round((times["async_overlap"] - times["gpu_only_unified"]) * 1e3, 3),
-        "hidden_fraction": round(max(0.0, times["sync_wait"] - times["async_overlap"])
-                                 / (layers * t_cpu), 3),
         "timing": f"wall clock over {iters} iterations after {warmup}",
     }
 
@@ -361,6 +371,8 @@ def main():
     ap.add_argument("--no-cpu-attention", action="store_true",
                     help="skip the host backend line")
     ap.add_argument("--no-overlap", action="store_true", help="skip the overlap runtime line")
+    ap.add_argument("--overlap-sweep", action="store_true",
+                    help="only run the overlap measurement over host-attended batch sizes")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -400,6 +412,11 @@ def main():
 
     log(f"generating workload {args.workload}")
     wl = W.DeviceWorkload(args.workload)
+    if args.overlap_sweep:
+        for b_cpu, l_cpu in ((8, 512), (16, 512), (32, 512), (64, 512), (16, 2048), (32, 2048)):
+            r = measure_overlap(A, torch, wl, b_cpu=b_cpu, l_cpu=l_cpu)
+            print(json.dumps(r), flush=True)
+        return
     cfg = wl.cfg
     nbytes = wl.algorithmic_bytes
     torch.cuda.synchronize()

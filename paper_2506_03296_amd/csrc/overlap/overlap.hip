@@ -12,6 +12,7 @@
 // come after the previous result has left the staging buffer.
 #include <hip/hip_runtime.h>
 
+#include <sched.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -40,6 +41,8 @@ __attribute__((format(printf, 2, 3))) int fail(int code, const char* fmt, ...)
 }
 
 enum SlotState : int { kFree = 0, kQueued = 1, kDone = 2, kCollected = 3 };
+
+constexpr int kSpinPolls = 2000;   // event queries (with a yield) before sleeping on it
 
 struct Slot {
     uint16_t* q = nullptr;     // pinned: [B][Hq][d] q, then [B][Hkv][d] kn and vn
@@ -81,9 +84,21 @@ struct apex_overlap {
     size_t kv_bytes(int B) const { return (size_t)B * cfg.Hkv * cfg.d * 2; }
     size_t cache_bytes() const { return (size_t)cfg.num_blocks * cfg.Hkv * cfg.block_size * cfg.d * 2; }
 
+    // Waits for the copies of a job: polls briefly (the GPU is usually about
+    // to deliver), then sleeps on the event.
+    static hipError_t wait_copies(hipEvent_t ev)
+    {
+        for (int i = 0; i < kSpinPolls; ++i) {
+            const hipError_t e = hipEventQuery(ev);
+            if (e != hipErrorNotReady) return e;
+            sched_yield();
+        }
+        return hipEventSynchronize(ev);
+    }
+
     void run_job(Slot& s)
     {
-        hipError_t e = hipEventSynchronize(s.in_done);
+        hipError_t e = wait_copies(s.in_done);
         if (e != hipSuccess) {
             s.rc = APEX_ERR_HIP;
             snprintf(s.msg, sizeof(s.msg), "copy of the new rows to the host failed: %s", hipGetErrorString(e));
