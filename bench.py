@@ -58,7 +58,7 @@ METRIC = "decode-attn µs/layer-step + achieved HBM GB/s (% peak), Llama-3.1-8B 
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
 # the files that define the attention kernel and its work partition: counter
-# summaries stay valid while these are unchanged
+# summaries stay valid while their code (comments aside) is unchanged
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2506_03296_amd", "csrc", f)
                   for f in ("kernels.h", "plan_policy.h")]
 
@@ -67,11 +67,20 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def _code_only(text):
+    """C++ source without comments and with whitespace runs collapsed, so that
+    editing a comment does not invalidate a counter summary."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_source_digest():
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p) as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -1,14 +1,16 @@
 // kernels.h -- gfx950 kernel of batched paged decode attention.
 //
-// One call = one launch of attn_kernel<G> on a persistent grid of W work
-// groups (4 waves each).  Every work group
+// One call = one launch of attn_kernel<G, kCheck> on a persistent grid of W
+// work groups (4 waves each); kCheck adds the optional input check (block ids
+// against the pool, contexts against an explicit table row).  Every work
+// group
 //   1. reads context_lens once and derives the partition of plan_policy.h on
 //      its own (block sums, a prefix scan, the longest request for the tight
 //      block-table stride), so no planner kernel runs before it;
 //   2. walks its contiguous range of (request b, kv-head g, block) units
 //      segment by segment.  In a segment the four waves take the blocks of
 //      one (b, g) pair round-robin; per 16-token block a wave gathers the
-//      paged K/V rows with 128-bit loads (prefetching its next block),
+//      paged K/V rows with 128-bit loads (two blocks in flight per wave),
 //      computes the G q-heads' scores as S^T = K Q^T with four
 //      16x16x32 fp16 MFMAs (q-heads padded to 16 columns), runs an online
 //      softmax (running max and sum in base 2, log2(e) folded into the
