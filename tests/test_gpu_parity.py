@@ -338,3 +338,44 @@ def test_checked_path_cuts_a_context_to_its_table_row(torch_cuda, apex, oracle_m
     ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
                                           case.context_lens, case.scale)
     assert_parity(got, ref, "context cut to the row")
+
+
+# ---------------------------------------------------------------------------
+# seeded random sweep: group sizes, length mixes (empty, one token, block
+# boundaries, long), table strides, worker counts and the checked path
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_configurations(torch_cuda, apex, oracle_mod, seed):
+    rng = np.random.default_rng(1000 + seed)
+    G = int(rng.choice([1, 2, 4, 8]))
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    B = int(rng.integers(1, 40))
+    kinds = rng.choice(["short", "edge", "long", "zero"], size=B, p=[0.4, 0.3, 0.2, 0.1])
+    lens = []
+    for k in kinds:
+        if k == "short":
+            lens.append(int(rng.integers(1, 64)))
+        elif k == "edge":
+            lens.append(int(16 * rng.integers(1, 40) + rng.choice([-1, 0, 1])))
+        elif k == "long":
+            lens.append(int(rng.integers(1000, 6000)))
+        else:
+            lens.append(0)
+    maxb = max([1] + [-(-L // 16) for L in lens])
+    stride = int(maxb + rng.integers(0, 5)) if rng.random() < 0.4 else None
+    case = W.make_host_case(lens, G * Hkv, Hkv, seed=seed, poison=True, stride=stride)
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale)
+    workers = int(rng.choice([0, 0, 1, 13, 300]))
+    kw = dict(num_workers=workers)
+    if stride is not None:
+        kw["block_table_stride"] = stride
+    if rng.random() < 0.3:
+        kw["check_inputs"] = True
+    print(f"[parity] seed={seed} G={G} Hkv={Hkv} B={B} stride={stride} {kw}", flush=True)
+    got = run_gpu(torch_cuda, apex, case, **kw)
+    assert_parity(got, ref, f"random seed={seed}")
+    assert np.all(got[np.asarray(lens) == 0] == 0)
+    if kw.get("check_inputs"):
+        assert apex.check_device_error() == 0
