@@ -15,7 +15,10 @@
 //      16x16x32 fp16 MFMAs (q-heads padded to 16 columns), runs an online
 //      softmax (running max and sum in base 2, log2(e) folded into the
 //      scale), and accumulates O^T += V^T P^T in fp32 with eight 16x16x16
-//      fp16 MFMAs, V^T being assembled in registers with byte permutes;
+//      fp16 MFMAs, V^T being assembled in registers with byte permutes.
+//      Each wave's K/V pipeline runs on across segments: between two long
+//      segments the last steps of one already load the next one's first
+//      blocks, and the next segment's Q operand is loaded one segment ahead;
 //   3. merges the waves' states in LDS and either writes the fp16 output rows
 //      (the segment is the whole pair) or stores an fp32 partial
 //      (accumulator, max, sum) and bumps the pair's arrival counter; the last
@@ -166,80 +169,174 @@ __device__ inline void load_slab(u32x4 (&w)[4], const f16* slab, int bytes, int 
         w[i] = __builtin_amdgcn_raw_buffer_load_b128(r, lane_off + stride * i, 0, kStreamingLoad);
 }
 
-// Per-wave attention over blocks lo + wave, lo + wave + 4, ... < hi of pair
-// (b, g).  Lane (h = lane % 16, q = lane / 16) keeps m (running max of head
-// h, log2 units, equal on the four lanes of h), l (sum of the weights of its
-// tokens) and acc[t][i] (running P.V of head h at dim 32q + 8i + t).  On
-// return the wave's state is in s_acc/s_m/s_l.
+// This wave's share of one segment (blocks lo..hi-1 of pair (b, g)): its
+// blocks are first, first + 4, ... < hi, n of them.  A wave with no block in
+// the segment, and the "next segment" after a work group's last one, have
+// n = 0.
+struct WaveSeg {
+    const int32_t* bt;   // block-table entry of the wave's first block
+    const f16* kpair;    // K / V of kv-head g in block 0 (a block id adds id * step)
+    const f16* vpair;
+    const f16* qrow;     // this lane's Q^T operand row (q-head g*G + lane % 16, if < G)
+    int first;           // the wave's first block (index into the pair's blocks)
+    int n;
+};
+
+template <int G>
+__device__ inline WaveSeg wave_seg(const AttnParams& p, const int32_t* bt_row, int b, int g, int lo,
+                                   int hi, int wave, int lane)
+{
+    WaveSeg s;
+    s.first = uniform(lo + wave);
+    s.n = s.first < hi ? (hi - s.first + kWaves - 1) / kWaves : 0;
+    s.bt = bt_row + s.first;
+    const size_t head_off = (size_t)uniform(g) * (kBlockSize * kHeadDim);
+    s.kpair = uniform_ptr(p.k + head_off);
+    s.vpair = uniform_ptr(p.v + head_off);
+    const int col = lane & 15;
+    s.qrow = p.q + ((size_t)b * p.Hq + (size_t)g * G + (col < G ? col : 0)) * kHeadDim + 8 * (lane >> 4);
+    return s;
+}
+
+// Q^T operand: lane (h, q) holds head h's dims [32i + 8q, +8) for MFMA i;
+// columns past the group are zero.
+template <int G>
+__device__ inline void load_q(f16x8 (&qop)[4], const WaveSeg& s, int lane)
+{
+    if ((lane & 15) < G) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) qop[i] = *(const f16x8*)(s.qrow + 32 * i);
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) qop[i] = f16x8{0, 0, 0, 0, 0, 0, 0, 0};
+    }
+}
+
+// The K/V pipeline of one wave, carried from segment to segment.  Tile t
+// (t = 0, 1) holds the wave's blocks of parity t.  When a segment and the next
+// both span at least kPrefetchBlocks blocks (every wave has at least four of
+// each), a segment's last two steps refill the tiles with the next segment's
+// blocks 0 and 1: they are in flight while the work group merges and emits
+// the segment, and the next segment starts with its first loads issued long
+// before.  Otherwise the next segment loads its first blocks itself.
+constexpr int kPrefetchBlocks = 16;
+
+struct WaveTiles {
+    u32x4 kt0[4], vt0[4], kt1[4], vt1[4];
+    int cur0, cur1;      // ids of the blocks in the tiles
+    int nid0, nid1;      // ids of the blocks that refill the tiles next
+    bool prefetched;     // the tiles hold the segment's blocks 0 and 1
+    f16x8 qop[4];        // Q^T of the current segment
+    f16x8 qnext[4];      // Q^T of the next segment (loaded one segment ahead)
+};
+
+// Per-wave attention over its blocks of segment cs; ns is the work group's
+// next segment (n = 0 if none), `safe` any readable block-table entry, pf_next
+// whether the tiles continue into ns.  Lane
+// (h = lane % 16, q = lane / 16) keeps m (running max of head h, log2 units,
+// equal on the four lanes of h), l (sum of the weights of its tokens) and
+// acc[t][i] (running P.V of head h at dim 32q + 8i + t).  On return the
+// wave's state is in s_acc/s_m/s_l and the tiles hold (in flight) the next
+// segment's first blocks.
 template <int G, bool kCheck>
-__device__ inline void wave_attend(const AttnParams& p, const int32_t* __restrict__ bt_row, int b,
-                                   int g, int L, int lo, int hi, int wave, int lane,
+__device__ inline void wave_attend(const AttnParams& p, const WaveSeg& cs, const WaveSeg& ns,
+                                   const int32_t* safe, bool pf_next, int L, WaveTiles& st, int wave,
+                                   int lane,
                                    float (*s_acc)[G][kHeadDim], float (*s_m)[G], float (*s_l)[G])
 {
     constexpr int D = kHeadDim;
     constexpr int BS = kBlockSize;
     const int col = lane & 15;
     const int q = lane >> 4;
+    const int n = cs.n;
 
-    // Q^T operand: lane (h, q) holds head h's dims [32i + 8q, +8) for MFMA i;
-    // columns past the group are zero
-    f16x8 qop[4];
-    if (col < G) {
-        const f16* qrow = p.q + ((size_t)b * p.Hq + (size_t)g * G + col) * D + 8 * q;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) qop[i] = *(const f16x8*)(qrow + 32 * i);
-    } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) qop[i] = f16x8{0, 0, 0, 0, 0, 0, 0, 0};
+    const uint32_t step = (uint32_t)((size_t)p.Hkv * BS * D);
+    const int koff = k_lane_offset(lane);
+    const int voff = v_lane_offset(lane);
+    // with the input check, a block id outside the pool is never read: its
+    // loads get a zero extent like those past the end
+    auto id_ok = [&](int id) -> bool { return !kCheck || (id >= 0 && (int64_t)id < p.num_blocks); };
+    // block id at position pos of this (here) or the next segment's wave
+    // list; `ok` false reads the safe entry (the id is then unused).  The
+    // table is read-only during the call: reading it through the constant
+    // address space keeps the load on the scalar path.
+    auto id_at = [&](bool here, int pos, bool ok) -> int {
+        const int32_t* a = ok ? (here ? cs.bt : ns.bt) + kWaves * pos : safe;
+        return *(const __attribute__((address_space(4))) int32_t*)a;
+    };
+    // the tiles continue into the next segment (the work group's choice:
+    // both segments are long)
+    const bool pf = pf_next;
+
+    if (!st.prefetched) {
+        // load the segment's blocks 0 and 1 (tile 0 first)
+        st.cur0 = id_at(true, 0, n > 0);
+        st.cur1 = id_at(true, 1, n > 1);
+        const int nb0 = n > 0 && id_ok(st.cur0) ? kSlabBytes : 0;
+        const int nb1 = n > 1 && id_ok(st.cur1) ? kSlabBytes : 0;
+        load_slab(st.kt0, cs.kpair + (uint64_t)(uint32_t)st.cur0 * step, nb0, koff, 64);
+        load_slab(st.vt0, cs.vpair + (uint64_t)(uint32_t)st.cur0 * step, nb0, voff, 256);
+        load_slab(st.kt1, cs.kpair + (uint64_t)(uint32_t)st.cur1 * step, nb1, koff, 64);
+        load_slab(st.vt1, cs.vpair + (uint64_t)(uint32_t)st.cur1 * step, nb1, voff, 256);
+        st.nid0 = id_at(true, 2, n > 2);
+        st.nid1 = id_at(true, 3, n > 3);
     }
+    // Everything loaded before the loop (the tiles, mostly issued during the
+    // previous segment's last steps, and this segment's Q^T, issued one
+    // segment ahead) is complete from here on, so the loop's own waits are
+    // those of its two-deep pipeline alone.
+    __builtin_amdgcn_s_waitcnt(0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) st.qop[i] = st.qnext[i];
+    load_q<G>(st.qnext, ns, lane);   // used by the next segment only
 
     float m = -INFINITY, l = 0.f;
     f32x4 acc[8];
 #pragma unroll
     for (int t = 0; t < 8; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // This wave's blocks are first + kWaves * k, k = 0 .. n - 1.  Two K/V
-    // tiles alternate and each step refills the tile it consumed with the
-    // block two steps ahead, so two blocks (16 KiB) stay in flight per wave.
-    // Slab addresses are formed in scalar registers only, block ids arrive
-    // through the scalar path (the table is a read-only restrict argument)
-    // ahead of use, and every step issues eight loads (zero-extent past the
-    // end) so the compiler can wait for exactly the oldest slab.
-    const int first = uniform(lo + wave);
-    const int n = first < hi ? (hi - first + kWaves - 1) / kWaves : 0;
-    const int32_t* __restrict__ bt_w = bt_row + first;
-    const size_t head_off = (size_t)uniform(g) * (BS * D);
-    const f16* kpair = uniform_ptr(p.k + head_off);
-    const f16* vpair = uniform_ptr(p.v + head_off);
-    const uint32_t step = (uint32_t)((size_t)p.Hkv * BS * D);
-    const int koff = k_lane_offset(lane);
-    const int voff = v_lane_offset(lane);
-    auto id_of = [&](int k) -> int { return k < n ? bt_w[kWaves * k] : 0; };
-    // with the input check, a block id outside the pool is never read: its
-    // loads get a zero extent like those past the end
-    auto id_ok = [&](int id) -> bool { return !kCheck || (id >= 0 && (int64_t)id < p.num_blocks); };
-    auto bytes_of = [&](int k, int id) -> int { return k < n && id_ok(id) ? kSlabBytes : 0; };
-
-    // One block: consume (kt, vt) holding block k (id cur), refill them with
-    // block k + 2 (id2).
-    auto block_step = [&](u32x4 (&kt)[4], u32x4 (&vt)[4], int k, int id2, int cur) {
-        const int nbytes = bytes_of(k + 2, id2);
-        const int tok0 = (first + kWaves * k) * BS;
-        if (kCheck && !id_ok(cur)) {
+    // One block: consume (kt, vt) holding block k (id cur) of tile t = k % 2,
+    // refill them with the tile's next element (id nid: this segment's block
+    // k + 2, else the next segment's block t), look up the id of the element
+    // after that.  Slab addresses are formed in scalar registers only, block
+    // ids arrive through the scalar path ahead of use, and every step issues
+    // eight loads (zero-extent when there is no element) so the compiler can
+    // wait for exactly the oldest slab.
+    auto block_step = [&](u32x4 (&kt)[4], u32x4 (&vt)[4], int k, int& cur, int& nid) {
+        const int t = k & 1;
+        // refill: this segment's block k + 2, else the next segment's block
+        // t (with pf), else nothing
+        const bool r_here = k + 2 < n;
+        const bool r_ok = r_here || pf;
+        // the id of the tile's element after that: block k + 4 here, else the
+        // next segment's block t or t + 2
+        const bool l_here = k + 4 < n;
+        const int l_pos = l_here ? k + 4 : (r_here ? t : t + 2);
+        const int id_next = id_at(l_here, l_pos, l_here || pf);
+        const int id2 = nid;
+        const f16* kbase = r_here ? cs.kpair : ns.kpair;
+        const f16* vbase = r_here ? cs.vpair : ns.vpair;
+        const int nbytes = r_ok && id_ok(id2) ? kSlabBytes : 0;
+        const int tok0 = (cs.first + kWaves * k) * BS;
+        const int cur_id = cur;
+        cur = id2;
+        nid = id_next;
+        if (kCheck && !id_ok(cur_id)) {
             // skip the block (its tokens take no part), keep the pipeline going
             if (lane == 0) report_error(p, kErrBlockId);
-            load_slab(kt, kpair + (uint64_t)(uint32_t)id2 * step, nbytes, koff, 64);
-            load_slab(vt, vpair + (uint64_t)(uint32_t)id2 * step, nbytes, voff, 256);
+            load_slab(kt, kbase + (uint64_t)(uint32_t)id2 * step, nbytes, koff, 64);
+            load_slab(vt, vbase + (uint64_t)(uint32_t)id2 * step, nbytes, voff, 256);
             return;
         }
-
         // S^T = K Q^T: lane (h, q) gets the scores of tokens 4q..4q+3 of head h
         f32x4 s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            s = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, kt[i]), qop[i], s, 0, 0, 0);
-        // K is consumed: refill it
-        load_slab(kt, kpair + (uint64_t)(uint32_t)id2 * step, nbytes, koff, 64);
+            s = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, kt[i]), st.qop[i], s, 0, 0, 0);
+        // K is consumed: refill it (in place: the barrier keeps the scheduler
+        // from issuing the loads above the products that read the tile)
+        __builtin_amdgcn_sched_barrier(0);
+        load_slab(kt, kbase + (uint64_t)(uint32_t)id2 * step, nbytes, koff, 64);
 
         float sv[4];
 #pragma unroll
@@ -273,8 +370,9 @@ __device__ inline void wave_attend(const AttnParams& p, const int32_t* __restric
             a[t][0] = pack_halves(vt[0][w], vt[1][w], sel);
             a[t][1] = pack_halves(vt[2][w], vt[3][w], sel);
         }
-        // V is consumed: refill it
-        load_slab(vt, vpair + (uint64_t)(uint32_t)id2 * step, nbytes, voff, 256);
+        // V is consumed: refill it (in place)
+        __builtin_amdgcn_sched_barrier(0);
+        load_slab(vt, vbase + (uint64_t)(uint32_t)id2 * step, nbytes, voff, 256);
         if (tail) {
             const bool ok0 = tok0 + 4 * q + 0 < L, ok1 = tok0 + 4 * q + 1 < L;
             const bool ok2 = tok0 + 4 * q + 2 < L, ok3 = tok0 + 4 * q + 3 < L;
@@ -297,24 +395,15 @@ __device__ inline void wave_attend(const AttnParams& p, const int32_t* __restric
         }
     };
 
-    u32x4 kt0[4], vt0[4], kt1[4], vt1[4];
-    int cur0 = id_of(0), cur1 = id_of(1);   // ids of the blocks in the two tiles
-    load_slab(kt0, kpair + (uint64_t)(uint32_t)cur0 * step, bytes_of(0, cur0), koff, 64);
-    load_slab(vt0, vpair + (uint64_t)(uint32_t)cur0 * step, bytes_of(0, cur0), voff, 256);
-    load_slab(kt1, kpair + (uint64_t)(uint32_t)cur1 * step, bytes_of(1, cur1), koff, 64);
-    load_slab(vt1, vpair + (uint64_t)(uint32_t)cur1 * step, bytes_of(1, cur1), voff, 256);
-    int ida = id_of(2), idb = id_of(3);   // ids of the blocks two steps ahead
-    for (int k = 0; k < n; k += 2) {
-        const int ida_next = id_of(k + 4);
-        block_step(kt0, vt0, k, ida, cur0);
-        cur0 = ida;
-        ida = ida_next;
-        if (k + 1 >= n) break;
-        const int idb_next = id_of(k + 5);
-        block_step(kt1, vt1, k + 1, idb, cur1);
-        cur1 = idb;
-        idb = idb_next;
+    // pairs of blocks, then an odd last block on tile 0 (a loop with a single
+    // exit keeps both tiles in the same registers from one segment to the next)
+    int k = 0;
+    for (; k + 1 < n; k += 2) {
+        block_step(st.kt0, st.vt0, k, st.cur0, st.nid0);
+        block_step(st.kt1, st.vt1, k + 1, st.cur1, st.nid1);
     }
+    if (k < n) block_step(st.kt0, st.vt0, k, st.cur0, st.nid0);
+    st.prefetched = pf;
 
     // the wave's state for head h: l summed over the four token groups
     float lw = l + wave_shfl_xor(l, 16);
@@ -452,12 +541,49 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     int blk = uniform((int)(off % nb));
     int64_t u = u0;
 
-    // 2. segments
+    // Moves a segment cursor past the `take` units of its segment; false when
+    // the worker's range is done.
+    auto advance = [&](int& b_, int64_t& pre_, int& L_, int& nb_, int& g_, int& blk_, int64_t& u_,
+                       int take_) -> bool {
+        u_ += take_;
+        if (u_ >= u1) return false;
+        blk_ += take_;
+        if (blk_ == nb_) {
+            blk_ = 0;
+            if (++g_ == p.Hkv) {
+                g_ = 0;
+                pre_ += nb_;
+                do {
+                    ++b_;
+                } while (b_ < B && len_of(b_) <= 0);
+                if (b_ >= B) return false;   // unreachable: units remain after the current pair
+                L_ = uniform(len_of(b_));
+                nb_ = (int)blocks_of(L_, kBlockSize);
+            }
+        }
+        return true;
+    };
+
+    // 2. segments.  Each one is announced to the waves together with the
+    // next, so their K/V pipelines run on from one to the other.
+    int take = (int)min((int64_t)(nb - blk), u1 - u);
+    WaveSeg cs = wave_seg<G>(p, bt + (size_t)uniform(b) * (size_t)stride, b, g, blk, blk + take, wave, lane);
+    WaveTiles st;
+    st.prefetched = false;
+    st.cur0 = st.cur1 = st.nid0 = st.nid1 = 0;
+    load_q<G>(st.qnext, cs, lane);
     while (true) {
-        const int take = (int)min((int64_t)(nb - blk), u1 - u);
-        const int lo = blk, hi = blk + take;
-        const int32_t* bt_row = bt + (size_t)uniform(b) * (size_t)stride;
-        wave_attend<G, kCheck>(p, bt_row, b, g, L, lo, hi, wave, lane, s_acc, s_m, s_l);
+        int b2 = b, L2 = L, nb2 = nb, g2 = g, blk2 = blk;
+        int64_t pre2 = pre, u2 = u;
+        const bool more = advance(b2, pre2, L2, nb2, g2, blk2, u2, take);
+        const int take2 = more ? (int)min((int64_t)(nb2 - blk2), u1 - u2) : 0;
+        WaveSeg ns = cs;
+        ns.n = 0;
+        if (more)
+            ns = wave_seg<G>(p, bt + (size_t)uniform(b2) * (size_t)stride, b2, g2, blk2, blk2 + take2, wave,
+                             lane);
+        wave_attend<G, kCheck>(p, cs, ns, bt, more && take >= kPrefetchBlocks && take2 >= kPrefetchBlocks,
+                               L, st, wave, lane, s_acc, s_m, s_l);
         __syncthreads();
 
         // 3. merge the waves, emit rows or a partial
@@ -546,22 +672,16 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         }
         __syncthreads();
 
-        u += take;
-        if (u >= u1) break;
-        blk = hi;
-        if (blk == nb) {
-            blk = 0;
-            if (++g == p.Hkv) {
-                g = 0;
-                pre += nb;
-                do {
-                    ++b;
-                } while (b < B && len_of(b) <= 0);
-                if (b >= B) break;   // unreachable: units remain after the current pair
-                L = uniform(len_of(b));
-                nb = (int)blocks_of(L, kBlockSize);
-            }
-        }
+        if (!more) break;
+        b = b2;
+        pre = pre2;
+        L = L2;
+        nb = nb2;
+        g = g2;
+        blk = blk2;
+        u = u2;
+        take = take2;
+        cs = ns;
     }
     }
 
