@@ -341,6 +341,62 @@ def test_checked_path_cuts_a_context_to_its_table_row(torch_cuda, apex, oracle_m
 
 
 # ---------------------------------------------------------------------------
+# the waves' K/V pipelines run on from segment to segment: when a segment and
+# the next both span >= 16 blocks, the next one's first two blocks per wave
+# (its blocks 0..7) are loaded during the current one's last steps
+# ---------------------------------------------------------------------------
+
+CHAIN_LENS = [15 * 16, 16 * 16, 17 * 16, 16 * 16 - 5, 33 * 16, 4 * 16, 64 * 16 + 3, 16 * 16, 1, 0, 31 * 16]
+
+
+@pytest.mark.parametrize("workers", [1, 2, 3, 5, 0])
+def test_segments_around_the_prefetch_length(torch_cuda, apex, oracle_mod, workers):
+    """Whole pairs of 15, 16 and 17 blocks back to back on one work group
+    (workers = 1: every transition is a prefetch decision), and splits of the
+    same batch at arbitrary points (workers = 2, 3, 5) and the default grid."""
+    case = W.make_host_case(CHAIN_LENS, 8, 2, seed=95, poison=True)
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale)
+    got = run_gpu(torch_cuda, apex, case, num_workers=workers)
+    assert_parity(got, ref, f"chained segments, workers={workers}")
+
+
+def drop_blocks(row, L, bad):
+    """Table row and length of the same request with the blocks at positions
+    `bad` removed (their tokens take no part; later blocks move up)."""
+    nb = -(-L // 16)
+    keep = [p for p in range(nb) if p not in bad]
+    toks = sum(min(16, L - 16 * p) for p in keep)
+    out = np.zeros_like(row)
+    out[:len(keep)] = row[keep]
+    return out, toks
+
+
+@pytest.mark.parametrize("workers", [1, 3, 0])
+def test_checked_path_bad_ids_at_prefetched_blocks(torch_cuda, apex, oracle_mod, workers):
+    """Block ids outside the pool at the positions the previous segment
+    prefetches (each wave's first two blocks: positions 0..7 of a segment)."""
+    lens = [40 * 16, 20 * 16 + 7, 16 * 16, 33 * 16]
+    case = W.make_host_case(lens, 8, 2, seed=96, poison=True)
+    nb = case.k_cache.shape[0]
+    bad = {0: [0, 5], 1: [1, 20], 2: [7], 3: [0, 1, 2, 3]}
+    bt = case.block_table.copy()
+    for b, ps in bad.items():
+        for p in ps:
+            bt[b, p] = nb + 11 * (p + 1)
+    bad_case = W.HostCase(case.q, case.k_cache, case.v_cache, bt, case.context_lens, case.scale)
+    exp_bt = case.block_table.copy()
+    exp_lens = case.context_lens.copy()
+    for b, ps in bad.items():
+        exp_bt[b], exp_lens[b] = drop_blocks(case.block_table[b], int(lens[b]), set(ps))
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, exp_bt, exp_lens,
+                                          case.scale)
+    got = run_gpu(torch_cuda, apex, bad_case, num_workers=workers, check_inputs=True)
+    assert apex.check_device_error() == apex.DEVICE_ERR_BLOCK_ID
+    assert_parity(got, ref, f"bad ids at prefetched blocks, workers={workers}")
+
+
+# ---------------------------------------------------------------------------
 # seeded random sweep: group sizes, length mixes (empty, one token, block
 # boundaries, long), table strides, worker counts and the checked path
 # ---------------------------------------------------------------------------
