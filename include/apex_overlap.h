@@ -32,7 +32,11 @@
  * The host KV cache of layer l ([num_blocks][Hkv][block_size][d] fp16, K and
  * V) is owned by the runtime (pinned, hipHostMalloc) and reachable through
  * apex_overlap_host_cache for filling it (e.g. with KV swapped out of the
- * GPU).  The attention is the one of apex_cpu_attention.h.
+ * GPU).  The compute thread appends to a layer's cache while that layer has
+ * jobs pending (apex_overlap_pending, or after apex_overlap_hold): write into
+ * it only when none is.  The attention is the one of apex_cpu_attention.h
+ * (its supported set -- d a multiple of 16 up to 512, G <= 64 -- is checked
+ * at create).
  *
  * Every layer has `slots_per_layer` result slots (default 2: one result in
  * flight while the next iteration submits).  A slot can be reused as soon as

@@ -232,7 +232,10 @@ int apex_overlap_create(const apex_overlap_config* cfg, apex_overlap** out)
     if (c.layers <= 0 || c.layers > 0xffff) return fail(APEX_ERR_INVALID_ARG, "layers must be in [1, 65535]");
     if (c.max_requests <= 0) return fail(APEX_ERR_INVALID_ARG, "max_requests must be positive");
     if (c.Hq <= 0 || c.Hkv <= 0 || c.Hq % c.Hkv != 0) return fail(APEX_ERR_INVALID_ARG, "bad head counts");
+    // the host attention's supported set (apex_cpu_attention.h), checked here
+    // so that a runtime which cannot serve any job is never created
     if (c.d <= 0 || c.d % 16 != 0 || c.d > 512) return fail(APEX_ERR_UNSUPPORTED, "head dim %d unsupported", c.d);
+    if (c.Hq / c.Hkv > 64) return fail(APEX_ERR_UNSUPPORTED, "group size %d above 64", c.Hq / c.Hkv);
     if (c.block_size <= 0 || c.num_blocks <= 0 || c.max_blocks_per_request <= 0)
         return fail(APEX_ERR_INVALID_ARG, "block_size, num_blocks and max_blocks_per_request must be positive");
     if (c.threads < 0 || c.slots_per_layer < 0) return fail(APEX_ERR_INVALID_ARG, "threads and slots must be >= 0");

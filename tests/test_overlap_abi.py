@@ -57,6 +57,12 @@ def test_bad_config_is_rejected_before_any_hip_call(lib, field, value, code):
     assert ov.last_error() != ""
 
 
+def test_group_size_beyond_the_host_backend_is_rejected(lib):
+    with pytest.raises(ov.OverlapError) as e:
+        ov.Overlap(**dict(BASE, Hq=128, Hkv=1))
+    assert e.value.code == -2
+
+
 def test_null_runtime_calls(lib):
     import ctypes
     assert lib.apex_overlap_destroy(None) == 0
