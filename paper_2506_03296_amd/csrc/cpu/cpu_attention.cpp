@@ -320,28 +320,28 @@ int run(const apex_cpu_args& a)
     });
 
     if (!splits.empty()) {
+        // the chunks of a split occupy consecutive partial slots; the pointer
+        // arrays are built here so that the workers allocate nothing
+        std::vector<const float*> ms((size_t)slots), ls((size_t)slots), accs((size_t)slots);
+        for (int64_t i = 0; i < slots; ++i) {
+            const float* base = partials + i * per_state;
+            ms[(size_t)i] = base;
+            ls[(size_t)i] = base + G;
+            accs[(size_t)i] = base + 2 * G;
+        }
         std::atomic<int64_t> next_split(0);
         const int64_t n_splits = (int64_t)splits.size();
         g_pool.run(threads, [&](int tid) {
             float* merged = g_thread_scratch.data() + scratch_each * tid;
-            std::vector<const float*> ms, ls, accs;
             for (;;) {
                 const int64_t i = next_split.fetch_add(1, std::memory_order_relaxed);
                 if (i >= n_splits) break;
                 const Split& s = splits[(size_t)i];
-                ms.clear();
-                ls.clear();
-                accs.clear();
-                for (int c = 0; c < s.chunks; ++c) {
-                    const float* base = partials + (s.first_slot + c) * per_state;
-                    ms.push_back(base);
-                    ls.push_back(base + G);
-                    accs.push_back(base + 2 * G);
-                }
+                const size_t f = (size_t)s.first_slot;
                 float* mm = merged;
                 float* ll = merged + G;
                 float* aa = merged + 2 * G;
-                K.merge(ms.data(), ls.data(), accs.data(), s.chunks, G, d, mm, ll, aa);
+                K.merge(&ms[f], &ls[f], &accs[f], s.chunks, G, d, mm, ll, aa);
                 const int64_t row = (int64_t)s.b * Hq + (int64_t)s.g * G;
                 K.finish(mm, ll, aa, G, d, out + row * d, lse ? lse + row : nullptr);
             }
