@@ -132,6 +132,28 @@ def cpu_baseline(wl, target_s):
     }
 
 
+def host_info():
+    """The host the CPU legs ran on: model, sockets, NUMA nodes, cores usable."""
+    model, sockets = "unknown", set()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                key, _, val = line.partition(":")
+                key = key.strip()
+                if key == "model name" and model == "unknown":
+                    model = val.strip()
+                elif key == "physical id":
+                    sockets.add(val.strip())
+    except OSError:
+        pass
+    try:
+        numa = len([d for d in os.listdir("/sys/devices/system/node") if d.startswith("node") and d[4:].isdigit()])
+    except OSError:
+        numa = None
+    return {"cpu_model": model, "sockets": len(sockets) or None, "numa_nodes": numa,
+            "cores_usable": len(os.sched_getaffinity(0)), "cores_online": os.cpu_count()}
+
+
 def time_append(A, torch, k_new, v_new, k_cache, v_cache, slots, reps):
     """Mean kernel time (ms) of apex_kv_append, from events around each call.
 
@@ -535,6 +557,8 @@ def main():
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    if not (args.no_cpu_baseline and args.no_cpu_attention and args.no_overlap):
+        result["host"] = host_info()
     print(json.dumps(result), flush=True)
 
 
