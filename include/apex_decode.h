@@ -74,7 +74,10 @@ typedef enum apex_status {
  * B == 0 is a successful no-op.  Uses library-owned workspaces, one set per
  * device, grown on demand (growing waits for the device); concurrent calls on
  * different streams of one device must use apex_decode_attention_ex with
- * caller-owned workspaces.
+ * caller-owned workspaces.  The call only enqueues one kernel (no host
+ * synchronisation, no memset; the arrival counters are left zero by every
+ * launch), so apex_decode_attention_ex with a caller workspace and no events
+ * can be captured in a HIP graph and replayed.
  */
 int apex_decode_attention(const void* q, const void* k_cache, const void* v_cache,
                           const int32_t* block_table, const int32_t* context_lens, void* out,
