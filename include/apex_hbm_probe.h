@@ -32,7 +32,9 @@ int apex_hbm_probe_stream(const void* buf, size_t bytes, int blocks, int flags, 
  * chunk_ids[i] * 4096 of `buf` (int32 ids, device memory), a 64-lane wave
  * per chunk with 128-bit loads, `blocks` work groups of 256 threads
  * (0 = 8 per compute unit).  flags bit 0 = non-temporal loads, bits 1-3 =
- * chunks each wave has in flight (1, 2 or 4). */
+ * chunks each wave has in flight (1, 2 or 4), bit 4 = the attention kernel's
+ * access form instead: a buffer resource per chunk and non-temporal buffer
+ * loads (bit 0 is then ignored). */
 int apex_hbm_probe_gather(const void* buf, const int32_t* chunk_ids, int64_t n_chunks, int blocks,
                           int flags, uint32_t* sink, void* stream);
 

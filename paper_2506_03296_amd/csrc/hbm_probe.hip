@@ -60,6 +60,41 @@ __global__ __launch_bounds__(256) void gather_kernel(const u32x4* __restrict__ p
     if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9e3779b9u) *sink = 1u;
 }
 
+// The same gather with the attention kernel's access form: per chunk a
+// buffer resource whose base is the chunk (4 KiB extent) and 128-bit
+// non-temporal buffer loads.
+constexpr int kRawBufferWord3 = 0x00020000;
+constexpr int kPolicy = 2;
+
+template <int U>
+__global__ __launch_bounds__(256) void gather_buffer_kernel(const unsigned char* __restrict__ p,
+                                                            const int32_t* __restrict__ ids,
+                                                            int64_t n_chunks, uint32_t* sink)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
+    int64_t w = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+    u32x4 acc = {0u, 0u, 0u, 0u};
+    for (; w < n_chunks; w += U * waves) {
+        u32x4 r[U][4];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t c = w + u * waves;
+            const int id = c < n_chunks ? __builtin_amdgcn_readfirstlane(ids[c]) : 0;
+            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                (void*)(p + (size_t)(uint32_t)id * 4096), (short)0, c < n_chunks ? 4096 : 0, kRawBufferWord3);
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                r[u][k] = __builtin_amdgcn_raw_buffer_load_b128(rs, lane * 16 + 1024 * k, 0, kPolicy);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) acc ^= r[u][k];
+    }
+    if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9e3779b9u) *sink = 1u;
+}
+
 int default_blocks(int blocks)
 {
     if (blocks > 0) return blocks;
@@ -91,7 +126,7 @@ int apex_hbm_probe_stream(const void* buf, size_t bytes, int blocks, int flags, 
 int apex_hbm_probe_gather(const void* buf, const int32_t* chunk_ids, int64_t n_chunks, int blocks,
                           int flags, uint32_t* sink, void* stream)
 {
-    if (!buf || !chunk_ids || !sink || n_chunks < 0 || blocks < 0 || (flags & ~0xf)) return -1;
+    if (!buf || !chunk_ids || !sink || n_chunks < 0 || blocks < 0 || (flags & ~0x1f)) return -1;
     const int unroll = (flags >> 1) & 7;
     if (unroll != 1 && unroll != 2 && unroll != 4) return -1;
     if (n_chunks == 0) return 0;
@@ -99,6 +134,15 @@ int apex_hbm_probe_gather(const void* buf, const int32_t* chunk_ids, int64_t n_c
     if (blocks <= 0) return -4;
     hipStream_t s = (hipStream_t)stream;
     const u32x4* p = (const u32x4*)buf;
+    if (flags & 16) {
+        const unsigned char* pb = (const unsigned char*)buf;
+        switch (unroll) {
+            case 1: gather_buffer_kernel<1><<<blocks, 256, 0, s>>>(pb, chunk_ids, n_chunks, sink); break;
+            case 2: gather_buffer_kernel<2><<<blocks, 256, 0, s>>>(pb, chunk_ids, n_chunks, sink); break;
+            default: gather_buffer_kernel<4><<<blocks, 256, 0, s>>>(pb, chunk_ids, n_chunks, sink); break;
+        }
+        return hipGetLastError() == hipSuccess ? 0 : -4;
+    }
     const bool nt = flags & 1;
     switch (unroll * 2 + (nt ? 1 : 0)) {
         case 2: gather_kernel<1, false><<<blocks, 256, 0, s>>>(p, chunk_ids, n_chunks, sink); break;

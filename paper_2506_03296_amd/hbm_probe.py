@@ -41,8 +41,10 @@ def _time(torch, fn, reps):
 
 
 def measure(nbytes=4 << 30, reps=10, blocks_list=(0,), seed=0):
-    """Returns GB/s per (pattern, flags, blocks): "stream" (flags = nt) and
-    "gather4k" (flags = nt | chunks-in-flight << 1)."""
+    """Returns GB/s per (pattern, flags, blocks): "stream" (flags = nt),
+    "gather4k" (flags = nt | chunks-in-flight << 1) and "gather4k_dev" (the
+    attention kernel's access form: a buffer resource per chunk,
+    non-temporal buffer loads)."""
     import torch
     lib = load_library()
     buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
@@ -53,7 +55,7 @@ def measure(nbytes=4 << 30, reps=10, blocks_list=(0,), seed=0):
     g.manual_seed(seed)
     ids = torch.randperm(n_chunks, generator=g, device="cuda").to(torch.int32)
     stream = torch.cuda.current_stream().cuda_stream
-    res = {"bytes": nbytes, "stream": {}, "gather4k": {}}
+    res = {"bytes": nbytes, "stream": {}, "gather4k": {}, "gather4k_dev": {}}
     for blocks in blocks_list:
         for nt in (0, 1):
             def f1():
@@ -69,4 +71,12 @@ def measure(nbytes=4 << 30, reps=10, blocks_list=(0,), seed=0):
                     assert rc == 0
                 res["gather4k"][f"nt{nt}_u{unroll}_wg{blocks}"] = round(
                     nbytes / _time(torch, f2, reps) / 1e9, 1)
+        for unroll in (1, 2, 4):
+            flags = 16 | (unroll << 1)
+
+            def f3():
+                rc = lib.apex_hbm_probe_gather(buf.data_ptr(), ids.data_ptr(), n_chunks, blocks,
+                                               flags, sink.data_ptr(), stream)
+                assert rc == 0
+            res["gather4k_dev"][f"u{unroll}_wg{blocks}"] = round(nbytes / _time(torch, f3, reps) / 1e9, 1)
     return res
