@@ -377,6 +377,31 @@ def measure_overlap(A, torch, wl, layers=8, b_cpu=16, l_cpu=512, iters=16, warmu
     }
 
 
+def measure_scheduler(wl, gpu_tokens, cpu_batch=16, cpu_tokens=16 * 4096, calls=20000):
+    """Alg. 2 of the library on inputs interpolated from the committed MI355X
+    profile (this GPU batch, a CPU batch of cpu_batch requests): the decision
+    and the host time per call through the binding (ctypes included)."""
+    from paper_2506_03296_amd import sched
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "sched_profile_mi355x.json")
+    with open(path) as f:
+        profile = json.load(f)
+    kw = sched.inputs_from_profile(profile, wl.cfg.B, gpu_tokens, cpu_batch, cpu_tokens)
+    r = sched.select(**kw)
+    t0 = time.perf_counter()
+    for _ in range(calls):
+        sched.select(**kw)
+    per = (time.perf_counter() - t0) / calls
+    return {
+        "algorithm": "Alg. 2 (decode), apex_sched_select",
+        "profile": "profiles/sched_profile_mi355x.json",
+        "gpu_batch": wl.cfg.B, "gpu_tokens": int(gpu_tokens), "cpu_batch": cpu_batch,
+        "cpu_tokens": cpu_tokens, "n_g_tokens_per_s": round(kw["n_g"], 1), "n_c_tokens_per_s": round(kw["n_c"], 1),
+        "ratio": round(kw["n_g"] / kw["n_c"], 2), "ratio_bound": round(r["ratio_bound"], 3),
+        "strategy": r["strategy"], "us_per_decision": round(per * 1e6, 3),
+        "timing": f"{calls} calls from Python, ctypes included",
+    }
+
+
 def _timed(fn):
     t0 = time.perf_counter()
     fn()
@@ -553,6 +578,8 @@ def main():
     if not args.no_overlap:
         log("timing the overlap runtime")
         result["overlap"] = measure_overlap(A, torch, wl)
+    log("timing the strategy selection")
+    result["scheduler"] = measure_scheduler(wl, int(wl.lens.sum()))
     if not args.no_append:
         log("timing kv_append")
         result["kv_append"] = measure_append(A, torch, W, wl, max(10, args.steps))
