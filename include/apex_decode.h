@@ -125,6 +125,18 @@ typedef struct apex_decode_args {
     uint32_t flags;
     /* physical blocks in k_cache/v_cache; needed by APEX_DECODE_FLAG_CHECK_INPUTS */
     int64_t num_blocks;
+    /* Fused append (both NULL = off): the current token's K and V rows, fp16
+     * [B][Hkv][d] with new_token_stride elements between tokens (0 = Hkv * d;
+     * otherwise a multiple of 8, >= Hkv * d), 16-byte aligned.  context_lens
+     * still counts the current token, but the caches need to hold only its
+     * first L_b - 1 tokens: the current token is attended from these rows and
+     * written to its slot -- the block_table entry of position L_b - 1, slot
+     * (L_b - 1) % block_size -- during the call (no request may share that
+     * slot).  Equivalent to apex_kv_append of these rows followed by the
+     * plain call, in one launch. */
+    const void* k_new;
+    const void* v_new;
+    int64_t new_token_stride;
 } apex_decode_args;
 
 /*

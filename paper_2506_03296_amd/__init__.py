@@ -61,6 +61,7 @@ class DecodeArgs(ctypes.Structure):
         ("workspace_bytes", ctypes.c_size_t), ("lse_out", ctypes.c_void_p),
         ("attn_kernel_events", ctypes.c_void_p * 2), ("flags", ctypes.c_uint32),
         ("num_blocks", ctypes.c_int64),
+        ("k_new", ctypes.c_void_p), ("v_new", ctypes.c_void_p), ("new_token_stride", ctypes.c_int64),
     ]
 
 
@@ -183,14 +184,18 @@ def decode_attention(q, k_cache, v_cache, block_table, context_lens, scale, out=
 
 def decode_attention_ex(q, k_cache, v_cache, block_table, context_lens, scale, out=None,
                         block_table_stride=0, num_workers=0, workspace=None,
-                        lse_out=None, events=None, stream=None, check_inputs=False):
+                        lse_out=None, events=None, stream=None, check_inputs=False,
+                        k_new=None, v_new=None):
     """apex_decode_attention_ex over torch tensors; returns ``out``.
 
     ``workspace`` is an optional uint8 device tensor (caller-owned; its first
     counter_bytes(B, Hkv) bytes must be zero, e.g. from torch.zeros);
     ``events`` an optional pair of torch.cuda.Event recorded around the
     attention kernel; ``check_inputs`` runs the input-checking kernel (block
-    ids against the caches' block count; see check_device_error)."""
+    ids against the caches' block count; see check_device_error);
+    ``k_new``/``v_new`` (fp16 [B][Hkv][d], unit strides inside a token) turn
+    on the fused append: the current token (position L - 1) is attended from
+    them and written to its cache slot in the same launch."""
     import torch
     B, Hq, Hkv, d, bs = _shapes(q, k_cache)
     if out is None:
@@ -214,6 +219,13 @@ def decode_attention_ex(q, k_cache, v_cache, block_table, context_lens, scale, o
     if check_inputs:
         a.flags = FLAG_CHECK_INPUTS
         a.num_blocks = k_cache.shape[0]
+    if k_new is not None or v_new is not None:
+        if k_new is None or v_new is None or k_new.shape != (B, Hkv, d) or v_new.shape != k_new.shape:
+            raise ValueError("k_new and v_new must both be [B][Hkv][d]")
+        if k_new.stride(2) != 1 or k_new.stride(1) != d or v_new.stride() != k_new.stride():
+            raise ValueError("k_new/v_new need unit strides inside a token and equal strides")
+        a.k_new, a.v_new = _addr(k_new), _addr(v_new)
+        a.new_token_stride = int(k_new.stride(0))
     _check(load_library().apex_decode_attention_ex(ctypes.byref(a)))
     return out
 

@@ -79,10 +79,10 @@ int resident_groups(int G, int* out)
     int n = 0;
     hipError_t e;
     switch (G) {
-        case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<1, false>, apex::kAttnThreads, 0); break;
-        case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<2, false>, apex::kAttnThreads, 0); break;
-        case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<4, false>, apex::kAttnThreads, 0); break;
-        default: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<8, false>, apex::kAttnThreads, 0); break;
+        case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<1, false, false>, apex::kAttnThreads, 0); break;
+        case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<2, false, false>, apex::kAttnThreads, 0); break;
+        case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<4, false, false>, apex::kAttnThreads, 0); break;
+        default: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, apex::attn_kernel<8, false, false>, apex::kAttnThreads, 0); break;
     }
     if (e != hipSuccess || n <= 0)
         return fail(APEX_ERR_HIP, "occupancy query failed: %s", hipGetErrorString(e));
@@ -166,7 +166,7 @@ int check_shapes(int B, int Hq, int Hkv, int d, int block_size)
     return APEX_OK;
 }
 
-template <int G, bool kCheck>
+template <int G, bool kCheck, bool kAppend>
 int launch(const apex::AttnParams& p, const int32_t* bt, const int32_t* lens, int64_t workers,
            void* const* events, hipStream_t stream)
 {
@@ -174,7 +174,7 @@ int launch(const apex::AttnParams& p, const int32_t* bt, const int32_t* lens, in
         hipError_t e = hipEventRecord((hipEvent_t)events[0], stream);
         if (e != hipSuccess) return fail(APEX_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
     }
-    apex::attn_kernel<G, kCheck><<<(unsigned)workers, apex::kAttnThreads, 0, stream>>>(p, bt, lens);
+    apex::attn_kernel<G, kCheck, kAppend><<<(unsigned)workers, apex::kAttnThreads, 0, stream>>>(p, bt, lens);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(APEX_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     if (events[1]) {
@@ -184,11 +184,34 @@ int launch(const apex::AttnParams& p, const int32_t* bt, const int32_t* lens, in
     return APEX_OK;
 }
 
+template <bool kCheck, bool kAppend>
+int dispatch_g(int G, const apex::AttnParams& p, const int32_t* bt, const int32_t* lens, int64_t workers,
+               void* const* ev, hipStream_t stream)
+{
+    switch (G) {
+        case 1: return launch<1, kCheck, kAppend>(p, bt, lens, workers, ev, stream);
+        case 2: return launch<2, kCheck, kAppend>(p, bt, lens, workers, ev, stream);
+        case 4: return launch<4, kCheck, kAppend>(p, bt, lens, workers, ev, stream);
+        default: return launch<8, kCheck, kAppend>(p, bt, lens, workers, ev, stream);
+    }
+}
+
+// One kernel build per (group size, input check, fused append): the default
+// path compiles without the other two.
+int dispatch(int G, bool check, bool append, const apex::AttnParams& p, const int32_t* bt,
+             const int32_t* lens, int64_t workers, void* const* ev, hipStream_t stream)
+{
+    if (check) return append ? dispatch_g<true, true>(G, p, bt, lens, workers, ev, stream)
+                             : dispatch_g<true, false>(G, p, bt, lens, workers, ev, stream);
+    return append ? dispatch_g<false, true>(G, p, bt, lens, workers, ev, stream)
+                  : dispatch_g<false, false>(G, p, bt, lens, workers, ev, stream);
+}
+
 }  // namespace
 
 extern "C" {
 
-int apex_decode_version(void) { return 300; }
+int apex_decode_version(void) { return 310; }
 
 const char* apex_decode_last_error(void) { return apex::last_error_message(); }
 
@@ -263,6 +286,17 @@ int apex_decode_attention_ex(const apex_decode_args* args)
     if (a.num_workers < 0 || a.num_workers > kMaxWorkers)
         return fail(APEX_ERR_INVALID_ARG, "num_workers = %d out of range", a.num_workers);
     if (a.block_table_stride < 0) return fail(APEX_ERR_INVALID_ARG, "block_table_stride is negative");
+    const bool append = a.k_new || a.v_new;
+    const int64_t new_row = (int64_t)a.Hkv * a.d;
+    const int64_t new_stride = a.new_token_stride ? a.new_token_stride : new_row;
+    if (append) {
+        if (!a.k_new || !a.v_new) return fail(APEX_ERR_INVALID_ARG, "the fused append needs both k_new and v_new");
+        if (new_stride < new_row || new_stride % 8 != 0)
+            return fail(APEX_ERR_INVALID_ARG, "new_token_stride %lld must be 0 or a multiple of 8 >= Hkv * d",
+                        (long long)a.new_token_stride);
+    } else if (a.new_token_stride != 0) {
+        return fail(APEX_ERR_INVALID_ARG, "new_token_stride without k_new/v_new");
+    }
     if (a.B == 0) return APEX_OK;
     if (!a.q || !a.k_cache || !a.v_cache || !a.block_table || !a.context_lens || !a.out)
         return fail(APEX_ERR_INVALID_ARG, "a tensor pointer is NULL");
@@ -277,6 +311,13 @@ int apex_decode_attention_ex(const apex_decode_args* args)
         return fail(APEX_ERR_INVALID_ARG, "out overlaps context_lens");
     if (a.lse_out && overlaps(a.lse_out, (size_t)a.B * a.Hq * 4, a.out, qo_bytes))
         return fail(APEX_ERR_INVALID_ARG, "lse_out overlaps out");
+    if (append) {
+        if (!aligned(a.k_new, 16) || !aligned(a.v_new, 16))
+            return fail(APEX_ERR_INVALID_ARG, "k_new and v_new must be 16-byte aligned");
+        const size_t new_bytes = ((size_t)(a.B - 1) * new_stride + new_row) * 2;
+        if (overlaps(a.out, qo_bytes, a.k_new, new_bytes) || overlaps(a.out, qo_bytes, a.v_new, new_bytes))
+            return fail(APEX_ERR_INVALID_ARG, "out overlaps k_new or v_new");
+    }
 
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
@@ -337,25 +378,17 @@ int apex_decode_attention_ex(const apex_decode_args* args)
     p.cus = cus;
     p.num_blocks = check ? a.num_blocks : 0;
     p.error_word = (unsigned*)error_word;
+    p.k_new = (const apex::f16*)a.k_new;
+    p.v_new = (const apex::f16*)a.v_new;
+    p.new_stride = new_stride;
+    p.k_store = (apex::f16*)a.k_cache;
+    p.v_store = (apex::f16*)a.v_cache;
 
     hipStream_t stream = (hipStream_t)a.stream;
     const int32_t* bt = a.block_table;
     const int32_t* lens = a.context_lens;
     void* const* ev = a.attn_kernel_events;
-    if (check) {
-        switch (G) {
-            case 1: return launch<1, true>(p, bt, lens, workers, ev, stream);
-            case 2: return launch<2, true>(p, bt, lens, workers, ev, stream);
-            case 4: return launch<4, true>(p, bt, lens, workers, ev, stream);
-            default: return launch<8, true>(p, bt, lens, workers, ev, stream);
-        }
-    }
-    switch (G) {
-        case 1: return launch<1, false>(p, bt, lens, workers, ev, stream);
-        case 2: return launch<2, false>(p, bt, lens, workers, ev, stream);
-        case 4: return launch<4, false>(p, bt, lens, workers, ev, stream);
-        default: return launch<8, false>(p, bt, lens, workers, ev, stream);
-    }
+    return dispatch(G, check, append, p, bt, lens, workers, ev, stream);
 }
 
 int apex_decode_attention(const void* q, const void* k_cache, const void* v_cache,

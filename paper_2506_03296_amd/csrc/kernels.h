@@ -1,8 +1,9 @@
 // kernels.h -- gfx950 kernel of batched paged decode attention.
 //
-// One call = one launch of attn_kernel<G, kCheck> on a persistent grid of W
-// work groups (4 waves each); kCheck adds the optional input check (block ids
-// against the pool, contexts against an explicit table row).  Every work
+// One call = one launch of attn_kernel<G, kCheck, kAppend> on a persistent
+// grid of W work groups (4 waves each); kCheck adds the optional input check
+// (block ids against the pool, contexts against an explicit table row),
+// kAppend the fused append of the current token's K/V.  Every work
 // group
 //   1. reads context_lens once and derives the partition of plan_policy.h on
 //      its own (block sums, a prefix scan, the longest request for the tight
@@ -66,6 +67,16 @@ struct AttnParams {
     int cus;               // compute units for the one-group-per-CU rule (0 = off)
     int64_t num_blocks;    // physical blocks in the caches (input check only)
     unsigned* error_word;  // input-check error bits (input check only)
+    // Fused append (optional): the current token's K/V rows, [B][Hkv][D] with
+    // new_stride elements between tokens.  The caches then hold the first
+    // L - 1 tokens of a request; the current one is attended from these rows
+    // and written to its slot (position L - 1) by the work group that emits
+    // the pair.
+    const f16* k_new;
+    const f16* v_new;
+    int64_t new_stride;
+    f16* k_store;          // the caches, written by the fused append
+    f16* v_store;
 };
 
 // Input-check error bits (apex_decode.h: APEX_DEVICE_ERR_*).
@@ -432,7 +443,53 @@ __device__ inline void write_row(const AttnParams& p, int b, int head, int dim, 
             den > 0.f ? (M + __log2f(den)) * 0.69314718055994531f : -INFINITY;
 }
 
-template <int G, bool kCheck>
+// Fused append.  Scaled logits (log2 units) of the current token for the G
+// q-heads of pair (b, g), computed by one wave (lane l takes dims 2l, 2l + 1).
+template <int G>
+__device__ inline void new_token_logits(const AttnParams& p, int b, int g, int lane, float* s_new)
+{
+    const f16x2 k2 = *(const f16x2*)(p.k_new + (size_t)b * p.new_stride + (size_t)g * kHeadDim + 2 * lane);
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        const f16x2 q2 = *(const f16x2*)(p.q + ((size_t)b * p.Hq + (size_t)g * G + h) * kHeadDim + 2 * lane);
+        float x = fmaf((float)q2[0], (float)k2[0], (float)q2[1] * (float)k2[1]);
+#pragma unroll
+        for (int m = 32; m >= 1; m >>= 1) x += wave_shfl_xor(x, m);
+        if (lane == 0) s_new[h] = x * p.scale_log2;
+    }
+}
+
+// Folds the current token (logit sn in log2 units, value vn) into a merged
+// state: running max M (log2 units; -inf when empty) and num, den relative
+// to it.  The weight is rounded to fp16 like the cached tokens' weights.
+__device__ inline void fold_new_token(float sn, float vn, float& M, float& num, float& den)
+{
+    const float M2 = fmaxf(M, sn);
+    const float r = M == -INFINITY ? 0.f : exp2_fast(M - M2);
+    const float wgt = (float)(f16)exp2_fast(sn - M2);
+    num = fmaf(wgt, vn, num * r);
+    den = fmaf(den, r, wgt);
+    M = M2;
+}
+
+// Writes element `dim` of the current token's K and V rows of kv-head g to
+// its cache slot: position Lc - 1 of request b (Lc = the full length).
+template <bool kCheck>
+__device__ inline void store_new_token(const AttnParams& p, const int32_t* bt_row, int b, int g, int Lc,
+                                       int dim)
+{
+    const int id = bt_row[(Lc - 1) / kBlockSize];
+    if (kCheck && !(id >= 0 && (int64_t)id < p.num_blocks)) {
+        if (dim == 0) report_error(p, kErrBlockId);
+        return;
+    }
+    const size_t dst = (((size_t)(uint32_t)id * p.Hkv + g) * kBlockSize + (Lc - 1) % kBlockSize) * kHeadDim + dim;
+    const size_t src = (size_t)b * p.new_stride + (size_t)g * kHeadDim + dim;
+    p.k_store[dst] = p.k_new[src];
+    p.v_store[dst] = p.v_new[src];
+}
+
+template <int G, bool kCheck, bool kAppend>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2))) void attn_kernel(AttnParams p,
                                                         const int32_t* __restrict__ bt,
                                                         const int32_t* __restrict__ lens)
@@ -448,6 +505,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     __shared__ int s_loc_b;
     __shared__ int64_t s_loc_pre;
     __shared__ int s_last;
+    __shared__ float s_new[G];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -469,14 +527,19 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     auto clamp_len = [&](int L) -> int {
         return kCheck && p.bt_stride > 0 && L > row_tokens ? (int)row_tokens : L;
     };
+    // with the fused append the partition covers the cached tokens, the
+    // first L - 1; the tight table stride still follows the full lengths
+    constexpr bool append = kAppend;
+    auto scan_len = [&](int Lc) -> int { return append && Lc > 0 ? Lc - 1 : Lc; };
     int tsum = 0, tmax = 0, tcnt = 0;
     for (int b = r0; b < r1; ++b) {
-        const int L = clamp_len(lens[b]);
-        if (kCheck && L != lens[b]) report_error(p, kErrTableRow);
+        const int Lc = clamp_len(lens[b]);
+        if (kCheck && Lc != lens[b]) report_error(p, kErrTableRow);
+        const int L = scan_len(Lc);
         if (cached) s_lens[b] = L;
         const int nb = (int)blocks_of(L, kBlockSize);
         tsum += nb;
-        tmax = max(tmax, nb);
+        tmax = max(tmax, (int)blocks_of(Lc, kBlockSize));
         tcnt += nb > 0;
     }
     int incl = tsum;
@@ -504,7 +567,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         maxb = max(maxb, s_wmax[v]);
         nonempty += s_wcnt[v];
     }
-    auto len_of = [&](int b) -> int { return cached ? s_lens[b] : clamp_len(lens[b]); };
+    auto len_of = [&](int b) -> int { return cached ? s_lens[b] : scan_len(clamp_len(lens[b])); };
 
     const int64_t units = (int64_t)uniform(total) * p.Hkv;
     const int64_t stride = p.bt_stride > 0 ? p.bt_stride : (int64_t)uniform(maxb);
@@ -584,6 +647,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
                              lane);
         wave_attend<G, kCheck>(p, cs, ns, bt, more && take >= kPrefetchBlocks && take2 >= kPrefetchBlocks,
                                L, st, wave, lane, s_acc, s_m, s_l);
+        if (append && wave == 0) new_token_logits<G>(p, b, g, lane, s_new);
         __syncthreads();
 
         // 3. merge the waves, emit rows or a partial
@@ -605,6 +669,11 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
                 den = fmaf(f, s_l[q][h], den);
             }
             if (wf == wl) {
+                if (append) {
+                    const size_t nrow = (size_t)b * p.new_stride + (size_t)g * D;
+                    fold_new_token(s_new[h], (float)p.v_new[nrow + dim], M, num, den);
+                    if (h == 0) store_new_token<kCheck>(p, bt + (size_t)b * stride, b, g, L + 1, dim);
+                }
                 write_row(p, b, g * G + h, dim, M, num, den);
             } else {
                 store_coherent(&p.pacc[((size_t)slot * G + h) * D + dim], num);
@@ -666,6 +735,11 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
                         }
                         M = Mn;
                     }
+                    if (append) {
+                        const size_t nrow = (size_t)b * p.new_stride + (size_t)g * D;
+                        fold_new_token(s_new[h], (float)p.v_new[nrow + dim], M, num, den);
+                        if (h == 0) store_new_token<kCheck>(p, bt + (size_t)b * stride, b, g, L + 1, dim);
+                    }
                     write_row(p, b, g * G + h, dim, M, num, den);
                 }
             }
@@ -685,9 +759,30 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     }
     }
 
-    // rows of empty requests are zeros (and lse = -inf)
+    // rows of empty requests are zeros (and lse = -inf); with the fused
+    // append a request whose only token is the current one returns its V row
+    // (lse = its scaled logit) and stores its K/V
     for (int b = (int)w; b < B; b += (int)gridDim.x) {
-        if (len_of(b) <= 0) {
+        if (len_of(b) > 0) continue;
+        if (append && clamp_len(lens[b]) == 1) {
+            const size_t nrow = (size_t)b * p.new_stride;
+            for (int i = tid; i < p.Hq * D; i += kAttnThreads) {
+                const int h = i / D, dim = i % D;
+                p.out[((size_t)b * p.Hq + h) * D + dim] = p.v_new[nrow + (size_t)(h / (p.Hq / p.Hkv)) * D + dim];
+            }
+            if (p.lse) {
+                for (int h = wave; h < p.Hq; h += kWaves) {
+                    const f16x2 k2 = *(const f16x2*)(p.k_new + nrow + (size_t)(h / (p.Hq / p.Hkv)) * D + 2 * lane);
+                    const f16x2 q2 = *(const f16x2*)(p.q + ((size_t)b * p.Hq + h) * D + 2 * lane);
+                    float x = fmaf((float)q2[0], (float)k2[0], (float)q2[1] * (float)k2[1]);
+#pragma unroll
+                    for (int m = 32; m >= 1; m >>= 1) x += wave_shfl_xor(x, m);
+                    if (lane == 0) p.lse[(size_t)b * p.Hq + h] = x * p.scale_log2 * 0.69314718055994531f;
+                }
+            }
+            for (int i = tid; i < p.Hkv * D; i += kAttnThreads)
+                store_new_token<kCheck>(p, bt + (size_t)b * stride, b, i / D, 1, i % D);
+        } else {
             for (int i = tid; i < p.Hq * D; i += kAttnThreads) write_row(p, b, i / D, i % D, 0.f, 0.f, 0.f);
         }
     }

@@ -240,6 +240,38 @@ def test_ex_check_flag_needs_the_block_count(lib):
     assert "num_blocks" in A.last_error()
 
 
+def _fake_args():
+    a = A.DecodeArgs()
+    a.q, a.k_cache, a.v_cache = FAKE, FAKE + (1 << 30), FAKE + (2 << 30)
+    a.block_table, a.context_lens, a.out = FAKE + (3 << 30), FAKE + (4 << 30), FAKE + (5 << 30)
+    a.B, a.Hq, a.Hkv, a.d, a.block_size, a.scale = 2, 32, 8, 128, 16, 0.1
+    return a
+
+
+@pytest.mark.parametrize("case", ["k_only", "v_only", "stride_alone", "stride_short", "stride_odd",
+                                  "misaligned", "out_overlaps_k_new"])
+def test_ex_fused_append_arguments(lib, case):
+    a = _fake_args()
+    if case == "k_only":
+        a.k_new = FAKE + (6 << 30)
+    elif case == "v_only":
+        a.v_new = FAKE + (6 << 30)
+    elif case == "stride_alone":
+        a.new_token_stride = 8 * 128
+    else:
+        a.k_new, a.v_new = FAKE + (6 << 30), FAKE + (7 << 30)
+        if case == "stride_short":
+            a.new_token_stride = 8 * 128 - 8
+        elif case == "stride_odd":
+            a.new_token_stride = 8 * 128 + 4
+        elif case == "misaligned":
+            a.k_new += 2
+        else:
+            a.k_new = a.out + 64
+    assert lib.apex_decode_attention_ex(ctypes.byref(a)) == A.APEX_ERR_INVALID_ARG
+    assert A.last_error() != ""
+
+
 def test_plan_host_rejects_bad_arguments(lib):
     with pytest.raises(A.ApexError):
         A.plan_host([5], 0, 256)

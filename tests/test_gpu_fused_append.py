@@ -1,0 +1,148 @@
+"""Fused append: apex_decode_attention_ex with k_new/v_new attends the current
+token (position L - 1) from the new rows and writes them to its cache slot in
+the same launch.
+
+Expected, from the oracles only: the KV append of oracle/kv_cache.py followed
+by the fp64 attention over the appended caches.  Outputs to the attention bar,
+the LSE to 2^-11 (see LSE_ABS), the caches bit for bit.  The current slots hold NaN in the
+caches before the call, so reading one instead of the new rows would show.
+"""
+import numpy as np
+import pytest
+
+import apex_workloads as W
+from oracle import kv_cache
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS = 2e-3
+REL_L2 = 1e-3
+# The LSE is log(sum of the weights) + max: the kernel rounds every weight to
+# fp16 (relative error <= 2^-11) and sums those same rounded weights, so with a
+# few comparable weights (contexts of 2-3 tokens here) the log of the sum is
+# off by up to 2^-11 ~ 4.9e-4; long contexts average it away.
+LSE_ABS = 2.0 ** -11
+D, BS = 128, 16
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+@pytest.fixture(scope="module")
+def apex():
+    import paper_2506_03296_amd as A
+    A.load_library()
+    return A
+
+
+def current_slots(case):
+    slots = np.full(len(case.context_lens), -1, dtype=np.int64)
+    for b, L in enumerate(case.context_lens):
+        if L > 0:
+            slots[b] = int(case.block_table[b, (L - 1) // BS]) * BS + (L - 1) % BS
+    return slots
+
+
+def fused_case(lens, G, Hkv, seed, stride=None):
+    case = W.make_host_case(lens, G * Hkv, Hkv, seed=seed, poison=True, stride=stride)
+    rng = np.random.default_rng(seed + 7)
+    B = len(lens)
+    kn = rng.standard_normal((B, Hkv, D)).astype(np.float16)
+    vn = rng.standard_normal((B, Hkv, D)).astype(np.float16)
+    slots = current_slots(case)
+    kc, vc = case.k_cache.copy(), case.v_cache.copy()
+    for s in slots[slots >= 0]:
+        kc[s // BS, :, s % BS, :] = np.float16(np.nan)
+        vc[s // BS, :, s % BS, :] = np.float16(np.nan)
+    exp_k, exp_v = kv_cache.kv_append(kc, vc, kn, vn, slots)
+    return case, kc, vc, kn, vn, exp_k, exp_v
+
+
+def check(got, ref, what):
+    got = np.asarray(got, dtype=np.float64)
+    assert np.all(np.isfinite(got)), what
+    err = float(np.abs(got - ref).max())
+    rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+    print(f"[fused] {what}: max_abs={err:.3e} rel_l2={rel:.3e}", flush=True)
+    assert err <= MAX_ABS and rel <= REL_L2, what
+
+
+LENS = [1, 2, 15, 16, 17, 33, 0, 500, 1024, 4096, 3]
+
+
+@pytest.mark.parametrize("G,Hkv", [(1, 8), (4, 8), (8, 2), (2, 4)])
+@pytest.mark.parametrize("workers", [0, 1, 3, 200])
+def test_fused_append_matches_append_then_attend(torch_cuda, apex, oracle_mod, G, Hkv, workers):
+    torch = torch_cuda
+    case, kc, vc, kn, vn, exp_k, exp_v = fused_case(LENS, G, Hkv, seed=101 + G * 10 + Hkv)
+    ref, lse_ref = oracle_mod.decode_attention_f64(case.q, exp_k, exp_v, case.block_table,
+                                                   case.context_lens, case.scale, return_lse=True)
+    dev = "cuda"
+    q = torch.from_numpy(case.q).to(dev)
+    kd, vd = torch.from_numpy(kc).to(dev), torch.from_numpy(vc).to(dev)
+    bt = torch.from_numpy(case.block_table).to(dev)
+    cl = torch.from_numpy(case.context_lens).to(dev)
+    lse = torch.empty((len(LENS), G * Hkv), dtype=torch.float32, device=dev)
+    out = apex.decode_attention_ex(q, kd, vd, bt, cl, case.scale, num_workers=workers, lse_out=lse,
+                                   k_new=torch.from_numpy(kn).to(dev), v_new=torch.from_numpy(vn).to(dev))
+    torch.cuda.synchronize()
+    check(out.cpu().numpy(), ref, f"G={G} Hkv={Hkv} workers={workers}")
+    assert np.all(out.cpu().numpy()[np.asarray(LENS) == 0] == 0)
+    got_lse = lse.cpu().numpy().astype(np.float64)
+    fin = np.isfinite(lse_ref)
+    assert np.all(np.isneginf(got_lse[~fin]))
+    assert np.max(np.abs(got_lse[fin] - lse_ref[fin])) <= LSE_ABS
+    assert np.array_equal(kd.cpu().numpy().view(np.uint16), exp_k.view(np.uint16))
+    assert np.array_equal(vd.cpu().numpy().view(np.uint16), exp_v.view(np.uint16))
+
+
+def test_fused_append_from_a_fused_qkv_buffer_and_wide_table(torch_cuda, apex, oracle_mod):
+    """k_new/v_new as views into one [B][Hq + 2 Hkv][d] projection output
+    (token stride wider than a row), with an explicit wide table stride."""
+    torch = torch_cuda
+    lens = [700, 17, 1, 64, 2000]
+    G, Hkv = 4, 8
+    stride = 140
+    case, kc, vc, kn, vn, exp_k, exp_v = fused_case(lens, G, Hkv, seed=131, stride=stride)
+    ref = oracle_mod.decode_attention_f64(case.q, exp_k, exp_v, case.block_table, case.context_lens,
+                                          case.scale)
+    dev = "cuda"
+    B, Hq = len(lens), G * Hkv
+    qkv = torch.zeros((B, Hq + 2 * Hkv, D), dtype=torch.float16, device=dev)
+    qkv[:, :Hq] = torch.from_numpy(case.q).to(dev)
+    qkv[:, Hq:Hq + Hkv] = torch.from_numpy(kn).to(dev)
+    qkv[:, Hq + Hkv:] = torch.from_numpy(vn).to(dev)
+    q = qkv[:, :Hq].contiguous()
+    kd, vd = torch.from_numpy(kc).to(dev), torch.from_numpy(vc).to(dev)
+    bt = torch.from_numpy(case.block_table).to(dev)
+    cl = torch.from_numpy(case.context_lens).to(dev)
+    out = apex.decode_attention_ex(q, kd, vd, bt, cl, case.scale, block_table_stride=stride,
+                                   k_new=qkv[:, Hq:Hq + Hkv], v_new=qkv[:, Hq + Hkv:])
+    torch.cuda.synchronize()
+    check(out.cpu().numpy(), ref, "fused qkv views")
+    assert np.array_equal(kd.cpu().numpy().view(np.uint16), exp_k.view(np.uint16))
+    assert np.array_equal(vd.cpu().numpy().view(np.uint16), exp_v.view(np.uint16))
+
+
+def test_fused_append_on_the_checked_path(torch_cuda, apex, oracle_mod):
+    torch = torch_cuda
+    lens = [40, 1, 300, 16]
+    case, kc, vc, kn, vn, exp_k, exp_v = fused_case(lens, 4, 8, seed=141)
+    ref = oracle_mod.decode_attention_f64(case.q, exp_k, exp_v, case.block_table, case.context_lens,
+                                          case.scale)
+    dev = "cuda"
+    kd, vd = torch.from_numpy(kc).to(dev), torch.from_numpy(vc).to(dev)
+    out = apex.decode_attention_ex(torch.from_numpy(case.q).to(dev), kd, vd,
+                                   torch.from_numpy(case.block_table).to(dev),
+                                   torch.from_numpy(case.context_lens).to(dev), case.scale,
+                                   check_inputs=True, k_new=torch.from_numpy(kn).to(dev),
+                                   v_new=torch.from_numpy(vn).to(dev))
+    torch.cuda.synchronize()
+    assert apex.check_device_error() == 0
+    check(out.cpu().numpy(), ref, "checked path")
+    assert np.array_equal(kd.cpu().numpy().view(np.uint16), exp_k.view(np.uint16))
