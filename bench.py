@@ -402,6 +402,47 @@ def measure_scheduler(wl, gpu_tokens, cpu_batch=16, cpu_tokens=16 * 4096, calls=
     }
 
 
+def measure_fused_step(A, torch, wl, steps=50, warmup=20):
+    """One layer-step as two launches (apex_kv_append, then the attention) and
+    as one fused call (k_new/v_new), back to back; the new rows are copies of
+    each request's last cached token, so the caches do not change."""
+    lens = wl.context_lens.to(torch.int64)
+    last = (lens - 1).clamp(min=0)
+    rows = torch.arange(wl.cfg.B, device=lens.device)
+    blocks = wl.block_table[rows, last // 16].to(torch.int64)
+    pos = last % 16
+    slots = torch.where(lens > 0, blocks * 16 + pos, torch.full_like(blocks, -1))
+    k_new = wl.k_cache[blocks, :, pos, :].contiguous()
+    v_new = wl.v_cache[blocks, :, pos, :].contiguous()
+
+    def separate():
+        A.kv_append(k_new, v_new, wl.k_cache, wl.v_cache, slots)
+        A.decode_attention(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens, wl.scale,
+                           out=wl.out)
+
+    def fused():
+        A.decode_attention_ex(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens, wl.scale,
+                              out=wl.out, k_new=k_new, v_new=v_new)
+
+    res = {}
+    for name, fn in (("separate", separate), ("fused", fused), ("separate_again", separate)):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        res[name] = a.elapsed_time(b) * 1e3 / steps
+    sep = (res["separate"] + res["separate_again"]) / 2
+    return {"us_per_step_append_then_attend": round(sep, 2), "us_per_step_fused": round(res["fused"], 2),
+            "saved_us": round(sep - res["fused"], 2),
+            "timing": f"{steps} back-to-back steps after {warmup}; the two-launch time is the mean of a run "
+                      "before and one after the fused run"}
+
+
 def _timed(fn):
     t0 = time.perf_counter()
     fn()
@@ -578,6 +619,8 @@ def main():
     if not args.no_overlap:
         log("timing the overlap runtime")
         result["overlap"] = measure_overlap(A, torch, wl)
+    log("timing the fused append")
+    result["fused_append"] = measure_fused_step(A, torch, wl)
     log("timing the strategy selection")
     result["scheduler"] = measure_scheduler(wl, int(wl.lens.sum()))
     if not args.no_append:
