@@ -191,6 +191,7 @@ struct WaveSeg {
     const f16* qrow;     // this lane's Q^T operand row (q-head g*G + lane % 16, if < G)
     int first;           // the wave's first block (index into the pair's blocks)
     int n;
+    int b, g;            // the pair
 };
 
 template <int G>
@@ -206,6 +207,8 @@ __device__ inline WaveSeg wave_seg(const AttnParams& p, const int32_t* bt_row, i
     s.vpair = uniform_ptr(p.v + head_off);
     const int col = lane & 15;
     s.qrow = p.q + ((size_t)b * p.Hq + (size_t)g * G + (col < G ? col : 0)) * kHeadDim + 8 * (lane >> 4);
+    s.b = b;
+    s.g = g;
     return s;
 }
 
@@ -241,6 +244,36 @@ struct WaveTiles {
     f16x8 qnext[4];      // Q^T of the next segment (loaded one segment ahead)
 };
 
+// Fused append.  Scaled logits (log2 units) of the current token for the G
+// q-heads of pair (b, g), computed by one wave (lane l takes dims 2l, 2l + 1):
+// the loads, then (once they are complete) the sums.
+template <int G>
+struct NewTokenRows {
+    f16x2 k2;
+    f16x2 q2[G];
+};
+
+template <int G>
+__device__ inline void load_new_token_rows(const AttnParams& p, int b, int g, int lane, NewTokenRows<G>& r)
+{
+    r.k2 = *(const f16x2*)(p.k_new + (size_t)b * p.new_stride + (size_t)g * kHeadDim + 2 * lane);
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+        r.q2[h] = *(const f16x2*)(p.q + ((size_t)b * p.Hq + (size_t)g * G + h) * kHeadDim + 2 * lane);
+}
+
+template <int G>
+__device__ inline void new_token_logits(const AttnParams& p, const NewTokenRows<G>& r, int lane, float* s_new)
+{
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        float x = fmaf((float)r.q2[h][0], (float)r.k2[0], (float)r.q2[h][1] * (float)r.k2[1]);
+#pragma unroll
+        for (int m = 32; m >= 1; m >>= 1) x += wave_shfl_xor(x, m);
+        if (lane == 0) s_new[h] = x * p.scale_log2;
+    }
+}
+
 // Per-wave attention over its blocks of segment cs; ns is the work group's
 // next segment (n = 0 if none), `safe` any readable block-table entry, pf_next
 // whether the tiles continue into ns.  Lane
@@ -249,11 +282,12 @@ struct WaveTiles {
 // acc[t][i] (running P.V of head h at dim 32q + 8i + t).  On return the
 // wave's state is in s_acc/s_m/s_l and the tiles hold (in flight) the next
 // segment's first blocks.
-template <int G, bool kCheck>
+template <int G, bool kCheck, bool kAppend>
 __device__ inline void wave_attend(const AttnParams& p, const WaveSeg& cs, const WaveSeg& ns,
                                    const int32_t* safe, bool pf_next, int L, WaveTiles& st, int wave,
                                    int lane,
-                                   float (*s_acc)[G][kHeadDim], float (*s_m)[G], float (*s_l)[G])
+                                   float (*s_acc)[G][kHeadDim], float (*s_m)[G], float (*s_l)[G],
+                                   float* s_new)
 {
     constexpr int D = kHeadDim;
     constexpr int BS = kBlockSize;
@@ -292,11 +326,20 @@ __device__ inline void wave_attend(const AttnParams& p, const WaveSeg& cs, const
         st.nid0 = id_at(true, 2, n > 2);
         st.nid1 = id_at(true, 3, n > 3);
     }
+    // with the fused append, wave 0 computes the current token's logits for
+    // this pair here, the loads of its rows sharing the wait below (the merge
+    // reads them).  Every wave issues those loads, a few hundred bytes: with
+    // a branch on the wave around them, the compiler's wait placement cannot
+    // tell that every path passes the wait, and the loop's first waits would
+    // then cover the tiles too.
+    NewTokenRows<G> nt;
+    if (kAppend) load_new_token_rows<G>(p, cs.b, cs.g, lane, nt);
     // Everything loaded before the loop (the tiles, mostly issued during the
     // previous segment's last steps, and this segment's Q^T, issued one
     // segment ahead) is complete from here on, so the loop's own waits are
     // those of its two-deep pipeline alone.
     __builtin_amdgcn_s_waitcnt(0);
+    if (kAppend && uniform(wave) == 0) new_token_logits<G>(p, nt, lane, s_new);
 #pragma unroll
     for (int i = 0; i < 4; ++i) st.qop[i] = st.qnext[i];
     load_q<G>(st.qnext, ns, lane);   // used by the next segment only
@@ -441,22 +484,6 @@ __device__ inline void write_row(const AttnParams& p, int b, int head, int dim, 
     if (p.lse && dim == 0)
         p.lse[(size_t)b * p.Hq + head] =
             den > 0.f ? (M + __log2f(den)) * 0.69314718055994531f : -INFINITY;
-}
-
-// Fused append.  Scaled logits (log2 units) of the current token for the G
-// q-heads of pair (b, g), computed by one wave (lane l takes dims 2l, 2l + 1).
-template <int G>
-__device__ inline void new_token_logits(const AttnParams& p, int b, int g, int lane, float* s_new)
-{
-    const f16x2 k2 = *(const f16x2*)(p.k_new + (size_t)b * p.new_stride + (size_t)g * kHeadDim + 2 * lane);
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-        const f16x2 q2 = *(const f16x2*)(p.q + ((size_t)b * p.Hq + (size_t)g * G + h) * kHeadDim + 2 * lane);
-        float x = fmaf((float)q2[0], (float)k2[0], (float)q2[1] * (float)k2[1]);
-#pragma unroll
-        for (int m = 32; m >= 1; m >>= 1) x += wave_shfl_xor(x, m);
-        if (lane == 0) s_new[h] = x * p.scale_log2;
-    }
 }
 
 // Folds the current token (logit sn in log2 units, value vn) into a merged
@@ -645,9 +672,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         if (more)
             ns = wave_seg<G>(p, bt + (size_t)uniform(b2) * (size_t)stride, b2, g2, blk2, blk2 + take2, wave,
                              lane);
-        wave_attend<G, kCheck>(p, cs, ns, bt, more && take >= kPrefetchBlocks && take2 >= kPrefetchBlocks,
-                               L, st, wave, lane, s_acc, s_m, s_l);
-        if (append && wave == 0) new_token_logits<G>(p, b, g, lane, s_new);
+        wave_attend<G, kCheck, kAppend>(p, cs, ns, bt,
+                                        more && take >= kPrefetchBlocks && take2 >= kPrefetchBlocks, L,
+                                        st, wave, lane, s_acc, s_m, s_l, s_new);
         __syncthreads();
 
         // 3. merge the waves, emit rows or a partial
