@@ -154,6 +154,20 @@ def _stream_handle(stream, device):
     return ctypes.c_void_p(_stream_obj(stream, device).cuda_stream)
 
 
+def _require(t, name, dtype, device, shape=None, contiguous=True):
+    """The library reads raw device pointers: a tensor of another dtype, on
+    the host or on another device, or with gaps would be read as garbage (or
+    fault the GPU), so such arguments are refused here."""
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, got {t.device}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if contiguous and not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
 def _shapes(q, k_cache):
     if q.dim() != 3 or k_cache.dim() != 4:
         raise ValueError("q must be [B][Hq][d] and the caches [num_blocks][Hkv][block_size][d]")
@@ -164,6 +178,28 @@ def _shapes(q, k_cache):
     return B, Hq, Hkv, d, bs
 
 
+def _check_tensors(q, k_cache, v_cache, block_table, context_lens, out, block_table_stride=0):
+    """dtype, device, shape and layout of the attention's tensors."""
+    import torch
+    B, Hq, Hkv, d, bs = _shapes(q, k_cache)
+    dev = q.device
+    if dev.type != "cuda":
+        raise ValueError(f"q must be a GPU tensor, got {dev}")
+    _require(q, "q", torch.float16, dev)
+    _require(k_cache, "k_cache", torch.float16, dev)
+    _require(v_cache, "v_cache", torch.float16, dev, shape=k_cache.shape)
+    _require(context_lens, "context_lens", torch.int32, dev, shape=(B,))
+    if block_table.dim() != 2 or block_table.shape[0] != B:
+        raise ValueError(f"block_table must be [B={B}][entries per row], got {tuple(block_table.shape)}")
+    if block_table_stride and block_table.shape[1] != block_table_stride:
+        raise ValueError(f"block_table rows hold {block_table.shape[1]} entries, "
+                         f"block_table_stride says {block_table_stride}")
+    _require(block_table, "block_table", torch.int32, dev)
+    if out is not None:
+        _require(out, "out", torch.float16, dev, shape=(B, Hq, d))
+    return B, Hq, Hkv, d, bs
+
+
 def decode_attention(q, k_cache, v_cache, block_table, context_lens, scale, out=None,
                      stream=None):
     """apex_decode_attention over torch tensors; returns ``out``.
@@ -171,7 +207,7 @@ def decode_attention(q, k_cache, v_cache, block_table, context_lens, scale, out=
     The block table must be tight ([B][ceil(max L / 16)]); use
     ``decode_attention_ex`` for wider rows."""
     import torch
-    B, Hq, Hkv, d, bs = _shapes(q, k_cache)
+    B, Hq, Hkv, d, bs = _check_tensors(q, k_cache, v_cache, block_table, context_lens, out)
     if out is None:
         out = torch.empty((B, Hq, d), dtype=torch.float16, device=q.device)
     lib = load_library()
@@ -197,9 +233,14 @@ def decode_attention_ex(q, k_cache, v_cache, block_table, context_lens, scale, o
     on the fused append: the current token (position L - 1) is attended from
     them and written to its cache slot in the same launch."""
     import torch
-    B, Hq, Hkv, d, bs = _shapes(q, k_cache)
+    B, Hq, Hkv, d, bs = _check_tensors(q, k_cache, v_cache, block_table, context_lens, out,
+                                       block_table_stride)
     if out is None:
         out = torch.empty((B, Hq, d), dtype=torch.float16, device=q.device)
+    if lse_out is not None:
+        _require(lse_out, "lse_out", torch.float32, q.device, shape=(B, Hq))
+    if workspace is not None:
+        _require(workspace, "workspace", torch.uint8, q.device)
     a = DecodeArgs()
     a.q, a.k_cache, a.v_cache = _addr(q), _addr(k_cache), _addr(v_cache)
     a.block_table, a.context_lens, a.out = _addr(block_table), _addr(context_lens), _addr(out)
@@ -222,6 +263,8 @@ def decode_attention_ex(q, k_cache, v_cache, block_table, context_lens, scale, o
     if k_new is not None or v_new is not None:
         if k_new is None or v_new is None or k_new.shape != (B, Hkv, d) or v_new.shape != k_new.shape:
             raise ValueError("k_new and v_new must both be [B][Hkv][d]")
+        _require(k_new, "k_new", torch.float16, q.device, contiguous=False)
+        _require(v_new, "v_new", torch.float16, q.device, contiguous=False)
         if k_new.stride(2) != 1 or k_new.stride(1) != d or v_new.stride() != k_new.stride():
             raise ValueError("k_new/v_new need unit strides inside a token and equal strides")
         a.k_new, a.v_new = _addr(k_new), _addr(v_new)
@@ -282,8 +325,15 @@ def kv_append(k_new, v_new, k_cache, v_cache, slot_mapping, stream=None):
             raise ValueError("each token's rows must be contiguous [Hkv][d]")
     if T > 1 and k_new.stride(0) != v_new.stride(0):
         raise ValueError("k_new and v_new must share the token stride")
-    if not (k_cache.is_contiguous() and v_cache.is_contiguous() and slot_mapping.is_contiguous()):
-        raise ValueError("caches and slot_mapping must be contiguous")
+    import torch
+    dev = k_cache.device
+    if dev.type != "cuda":
+        raise ValueError(f"the caches must be GPU tensors, got {dev}")
+    _require(k_cache, "k_cache", torch.float16, dev)
+    _require(v_cache, "v_cache", torch.float16, dev)
+    _require(k_new, "k_new", torch.float16, dev, contiguous=False)
+    _require(v_new, "v_new", torch.float16, dev, contiguous=False)
+    _require(slot_mapping, "slot_mapping", torch.int64, dev, shape=(T,))
     stride = k_new.stride(0) if T > 1 else 0
     rc = load_library().apex_kv_append(_ptr(k_new), _ptr(v_new), stride, _ptr(k_cache),
                                        _ptr(v_cache), _ptr(slot_mapping), T, Hkv, d, bs, nb,

@@ -111,6 +111,7 @@ class Overlap:
         h = ctypes.c_void_p()
         _check(self._lib.apex_overlap_create(ctypes.byref(self.cfg), ctypes.byref(h)))
         self._h = h
+        self._rows = {}   # ticket -> rows of its result, until collected
 
     def host_cache(self, layer):
         """(k, v) numpy float16 views [num_blocks][Hkv][block_size][d] of the
@@ -124,29 +125,64 @@ class Overlap:
         mv = np.ctypeslib.as_array(ctypes.cast(v, ctypes.POINTER(ctypes.c_uint16)), shape=(n,))
         return mk.view(np.float16).reshape(shape), mv.view(np.float16).reshape(shape)
 
+    def _check_rows(self, t, name, heads, B):
+        """q/k_new/v_new/out: contiguous fp16 GPU tensors [B][heads][d] (the
+        runtime copies them as raw device bytes)."""
+        import torch
+        if t.device.type != "cuda" or t.dtype != torch.float16 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float16 GPU tensor")
+        if tuple(t.shape) != (B, heads, self.cfg.d):
+            raise ValueError(f"{name} must have shape {(B, heads, self.cfg.d)}, got {tuple(t.shape)}")
+
     def submit(self, layer, q, k_new, v_new, slot_mapping, block_table, context_lens,
                stream=None, block_table_stride=0):
         slots = _host(slot_mapping, np.int64)
         table = _host(block_table, np.int32)
         lens = _host(context_lens, np.int32)
         B = int(q.shape[0])
+        self._check_rows(q, "q", self.cfg.Hq, B)
+        self._check_rows(k_new, "k_new", self.cfg.Hkv, B)
+        self._check_rows(v_new, "v_new", self.cfg.Hkv, B)
+        if slots.shape != (B,) or lens.shape != (B,):
+            raise ValueError(f"slot_mapping and context_lens must hold B = {B} entries")
+        if table.ndim != 2 or table.shape[0] != B:
+            raise ValueError(f"block_table must be [B = {B}][entries per row]")
+        if block_table_stride and block_table_stride != table.shape[1]:
+            raise ValueError("block_table_stride must equal the table's row length")
         t = ctypes.c_int64()
         _check(self._lib.apex_overlap_submit(
             self._h, layer, ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_new.data_ptr()),
             ctypes.c_void_p(v_new.data_ptr()), slots.ctypes.data, table.ctypes.data,
             int(block_table_stride or table.shape[1]), lens.ctypes.data, B,
             _stream(stream, q.device), ctypes.byref(t)))
+        self._rows[t.value] = B
         return t.value
 
     def poll(self, ticket, out, stream=None):
+        self._check_out(out, ticket)
         ready = ctypes.c_int()
         _check(self._lib.apex_overlap_poll(self._h, ticket, ctypes.c_void_p(out.data_ptr()),
                                            _stream(stream, out.device), ctypes.byref(ready)))
+        if ready.value:
+            self._rows.pop(ticket, None)
         return bool(ready.value)
 
     def wait(self, ticket, out, stream=None):
+        self._check_out(out, ticket)
         _check(self._lib.apex_overlap_wait(self._h, ticket, ctypes.c_void_p(out.data_ptr()),
                                            _stream(stream, out.device)))
+        self._rows.pop(ticket, None)
+
+    def _check_out(self, out, ticket):
+        """out receives the ticket's B rows [B][Hq][d] as raw device bytes."""
+        import torch
+        if out.device.type != "cuda" or out.dtype != torch.float16 or not out.is_contiguous():
+            raise ValueError("out must be a contiguous float16 GPU tensor")
+        if out.dim() != 3 or tuple(out.shape[1:]) != (self.cfg.Hq, self.cfg.d):
+            raise ValueError(f"out must be [B][{self.cfg.Hq}][{self.cfg.d}], got {tuple(out.shape)}")
+        rows = self._rows.get(ticket)
+        if rows is not None and out.shape[0] < rows:
+            raise ValueError(f"out holds {out.shape[0]} rows, the ticket's result has {rows}")
 
     def hold(self, flag=True):
         _check(self._lib.apex_overlap_hold(self._h, int(bool(flag))))

@@ -343,3 +343,44 @@ def test_kv_append_overlapping_fused_inputs_are_allowed(lib):
     base = FAKE
     kn, vn = base + Hq * d * 2, base + (Hq + Hkv) * d * 2
     assert append_call(lib, T=4, nb=0, stride=stride, kn=kn, vn=vn) == A.APEX_OK
+
+
+# ---------------------------------------------------------------------------
+# Python binding: tensors the library would misread are refused before the
+# call (no GPU needed: host tensors and the checking helper itself)
+# ---------------------------------------------------------------------------
+
+def test_binding_refuses_host_tensors():
+    torch = pytest.importorskip("torch")
+    q = torch.zeros((2, 8, 128), dtype=torch.float16)
+    kc = torch.zeros((4, 2, 16, 128), dtype=torch.float16)
+    bt = torch.zeros((2, 2), dtype=torch.int32)
+    lens = torch.tensor([5, 20], dtype=torch.int32)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        A.decode_attention(q, kc, kc.clone(), bt, lens, 0.1)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        A.decode_attention_ex(q, kc, kc.clone(), bt, lens, 0.1)
+    kn = torch.zeros((2, 2, 128), dtype=torch.float16)
+    with pytest.raises(ValueError, match="GPU tensors"):
+        A.kv_append(kn, kn.clone(), kc, kc.clone(), torch.tensor([0, 1]))
+
+
+@pytest.mark.parametrize("case", ["dtype", "device", "shape", "gaps"])
+def test_binding_tensor_check(case):
+    torch = pytest.importorskip("torch")
+    cpu = torch.device("cpu")
+    t = torch.zeros((4, 6), dtype=torch.float16)
+    if case == "dtype":
+        with pytest.raises(TypeError, match="must be torch.float16"):
+            A._require(t.float(), "x", torch.float16, cpu)
+    elif case == "device":
+        with pytest.raises(ValueError, match="must be on cuda:0"):
+            A._require(t, "x", torch.float16, torch.device("cuda", 0))
+    elif case == "shape":
+        with pytest.raises(ValueError, match=r"shape \(4, 5\)"):
+            A._require(t, "x", torch.float16, cpu, shape=(4, 5))
+    else:
+        with pytest.raises(ValueError, match="contiguous"):
+            A._require(t[:, ::2], "x", torch.float16, cpu)
+        A._require(t[:, ::2], "x", torch.float16, cpu, contiguous=False)
+    A._require(t, "x", torch.float16, cpu, shape=(4, 6))

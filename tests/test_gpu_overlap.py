@@ -223,6 +223,16 @@ def test_bad_arguments(torch_cuda, ov):
             rt.submit(0, q[:2], kn[:2], vn[:2], req.slots[:2], bad, req.lens[:2])
         with pytest.raises(OverlapError):
             rt.host_cache(2)
+        # refused in the binding: rows the runtime would copy as raw bytes
+        with pytest.raises(ValueError, match="q must be"):
+            rt.submit(0, q[:2].float(), kn[:2], vn[:2], req.slots[:2], req.layout.block_table[:2],
+                      req.lens[:2])
+        with pytest.raises(ValueError, match="context_lens must hold"):
+            rt.submit(0, q[:2], kn[:2], vn[:2], req.slots[:2], req.layout.block_table[:2], req.lens[:1])
+        t = rt.submit(0, q[:2], kn[:2], vn[:2], req.slots[:2], req.layout.block_table[:2], req.lens[:2])
+        with pytest.raises(ValueError, match="out holds 1 rows"):
+            rt.wait(t, torch.empty((1, 32, 128), dtype=torch.float16, device="cuda"))
+        rt.wait(t, torch.empty((2, 32, 128), dtype=torch.float16, device="cuda"))
 
 
 def test_destroy_with_pending_work_drains(torch_cuda, ov):

@@ -124,6 +124,35 @@ def test_wide_block_table_stride(torch_cuda, apex, oracle_mod):
     assert_parity(got, ref, "stride=64")
 
 
+def test_binding_refuses_tensors_the_library_would_misread(torch_cuda, apex):
+    """Checked in the binding before any launch: nothing runs on the GPU."""
+    torch = torch_cuda
+    case = W.make_host_case([40, 300, 17], 8, 2, seed=5, stride=64)
+    q, k, v, bt, lens = to_dev(torch, case)
+    s = case.scale
+    with pytest.raises(TypeError, match="q must be"):
+        apex.decode_attention(q.float(), k, v, bt, lens, s)
+    with pytest.raises(TypeError, match="context_lens must be"):
+        apex.decode_attention(q, k, v, bt, lens.long(), s)
+    with pytest.raises(ValueError, match="block_table must be on"):
+        apex.decode_attention(q, k, v, bt.cpu(), lens, s)
+    with pytest.raises(ValueError, match="k_cache must be contiguous"):
+        apex.decode_attention(q, k.transpose(2, 3).contiguous().transpose(2, 3), v, bt, lens, s)
+    with pytest.raises(ValueError, match="v_cache must have shape"):
+        apex.decode_attention(q, k, v[:-1], bt, lens, s)
+    with pytest.raises(ValueError, match="out must have shape"):
+        apex.decode_attention(q, k, v, bt, lens, s, out=torch.empty_like(q)[:2])
+    with pytest.raises(ValueError, match="block_table_stride says 32"):
+        apex.decode_attention_ex(q, k, v, bt, lens, s, block_table_stride=32)
+    with pytest.raises(TypeError, match="lse_out must be"):
+        apex.decode_attention_ex(q, k, v, bt, lens, s, block_table_stride=64,
+                                 lse_out=torch.empty((3, 8), dtype=torch.float16, device="cuda"))
+    kn = torch.zeros((3, 2, 128), dtype=torch.float16, device="cuda")
+    with pytest.raises(TypeError, match="slot_mapping must be"):
+        apex.kv_append(kn, kn.clone(), k, v, torch.zeros(3, dtype=torch.int32, device="cuda"))
+    torch.cuda.synchronize()
+
+
 def test_caller_workspace_and_side_stream(torch_cuda, apex, oracle_mod):
     torch = torch_cuda
     case = W.make_host_case([500, 5, 2000], 32, 8, seed=6)
