@@ -106,6 +106,33 @@ __device__ inline float exp2_fast(float x)
     return __builtin_amdgcn_exp2f(x);
 }
 
+// Inclusive prefix sum / max over the 64 lanes of a wave with DPP (row
+// shifts within each 16-lane row, then the row broadcasts of lanes 15 and 31
+// into the rows above): a few VALU cycles per step, where a cross-lane
+// shuffle goes through the LDS crossbar.  Lane 63 ends with the wave's total.
+__device__ inline int wave_incl_sum(int x)
+{
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);   // row_bcast:15, rows 1, 3
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);   // row_bcast:31, rows 2, 3
+    return x;
+}
+
+// As wave_incl_sum with max, for x >= 0.
+__device__ inline int wave_incl_max(int x)
+{
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false));
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false));
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false));
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false));
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false));
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false));
+    return x;
+}
+
 __device__ inline int uniform(int x)
 {
     return __builtin_amdgcn_readfirstlane(x);
@@ -569,19 +596,11 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         tmax = max(tmax, (int)blocks_of(Lc, kBlockSize));
         tcnt += nb > 0;
     }
-    int incl = tsum;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int y = __shfl_up(incl, d, 64);
-        if (lane >= d) incl += y;
-    }
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        tmax = max(tmax, __shfl_xor(tmax, d, 64));
-        tcnt += __shfl_xor(tcnt, d, 64);
-    }
-    if (lane == 63) s_wsum[wave] = incl;
-    if (lane == 0) {
+    int incl = wave_incl_sum(tsum);
+    tmax = wave_incl_max(tmax);
+    tcnt = wave_incl_sum(tcnt);
+    if (lane == 63) {
+        s_wsum[wave] = incl;
         s_wmax[wave] = tmax;
         s_wcnt[wave] = tcnt;
     }
@@ -627,8 +646,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     int L = uniform(len_of(b));
     int nb = (int)blocks_of(L, kBlockSize);
     int64_t off = u0 - pre * p.Hkv;
-    int g = uniform((int)(off / nb));
-    int blk = uniform((int)(off % nb));
+    const int64_t gq = div_floor(off, nb);
+    int g = uniform((int)gq);
+    int blk = uniform((int)(off - gq * nb));
     int64_t u = u0;
 
     // Moves a segment cursor past the `take` units of its segment; false when

@@ -26,6 +26,15 @@ constexpr int kBlockSize = 16;
 constexpr int kMinUnitsPerWorker = 8;   // two blocks per wave of a 4-wave work group
 constexpr int64_t kUnitsPerCuForOne = 1024;   // 8 MiB of K/V per CU
 
+// floor(a / b) for a >= 0, b > 0.  A 64-bit division is a long software
+// sequence on the GPU; the partition's operands nearly always fit in 32 bits,
+// where the hardware-assisted 32-bit sequence gives the same quotient.
+__host__ __device__ inline int64_t div_floor(int64_t a, int64_t b)
+{
+    if (((uint64_t)a | (uint64_t)b) <= 0xffffffffull) return (int64_t)((uint32_t)a / (uint32_t)b);
+    return a / b;
+}
+
 __host__ __device__ inline int64_t blocks_of(int32_t len, int bs)
 {
     return len > 0 ? ((int64_t)len + bs - 1) / bs : 0;
@@ -44,7 +53,7 @@ __host__ __device__ inline int64_t active_workers(int64_t units, int64_t launche
                                                   int64_t pairs, int64_t cus)
 {
     if (cus > 0 && pairs <= cus && units <= cus * kUnitsPerCuForOne && launched > cus) launched = cus;
-    int64_t w = units / (min_units > 0 ? min_units : 1);
+    int64_t w = div_floor(units, min_units > 0 ? min_units : 1);
     if (w < pairs) w = pairs;
     if (w < 1) w = 1;
     return w < launched ? w : launched;
@@ -53,13 +62,13 @@ __host__ __device__ inline int64_t active_workers(int64_t units, int64_t launche
 // First unit of worker w (the range of w is [worker_start(w), worker_start(w+1))).
 __host__ __device__ inline int64_t worker_start(int64_t w, int64_t units, int64_t workers)
 {
-    return (w * units) / workers;
+    return div_floor(w * units, workers);
 }
 
 // The worker whose range holds unit u (0 <= u < units).
 __host__ __device__ inline int64_t worker_of(int64_t u, int64_t units, int64_t workers)
 {
-    return ((u + 1) * workers - 1) / units;
+    return div_floor((u + 1) * workers - 1, units);
 }
 
 // Partial slot that worker w uses for the pair whose units start at p0:
