@@ -701,7 +701,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         const int64_t p0 = pre * p.Hkv + (int64_t)g * nb;
         const int64_t wf = worker_of(p0, units, W);
         const int64_t wl = worker_of(p0 + nb - 1, units, W);
-        const int64_t slot = partial_slot(w, p0, units, W);
+        const int64_t slot = u0 < p0 ? 2 * w + 1 : 2 * w;   // partial_slot(w, p0, units, W)
         for (int idx = tid; idx < G * D; idx += kAttnThreads) {
             const int h = idx / D, dim = idx % D;
             float M = s_m[0][h];
@@ -750,6 +750,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
                 // kCombineChunk contributors at once, then folds them in with
                 // an online rescale (running max M, numerator, denominator)
                 const int nc = (int)(wl - wf + 1);
+                // every contributor after the first starts inside the pair,
+                // so its slot is 2v (its first segment)
+                const int64_t first_slot = partial_slot(wf, p0, units, W);
                 for (int idx = tid; idx < G * D; idx += kAttnThreads) {
                     const int h = idx / D, dim = idx % D;
                     float M = -INFINITY, num = 0.f, den = 0.f;
@@ -761,7 +764,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
                             cl[j] = 0.f;
                             ca[j] = 0.f;
                             if (c0 + j < nc) {
-                                const int64_t sq = partial_slot(wf + c0 + j, p0, units, W);
+                                const int64_t sq = c0 + j == 0 ? first_slot : 2 * (wf + c0 + j);
                                 cm[j] = load_coherent(&p.pml[((size_t)sq * G + h) * 2]);
                                 cl[j] = load_coherent(&p.pml[((size_t)sq * G + h) * 2 + 1]);
                                 ca[j] = load_coherent(&p.pacc[((size_t)sq * G + h) * D + dim]);
