@@ -121,6 +121,18 @@ __device__ inline int wave_incl_sum(int x)
     return x;
 }
 
+// As wave_incl_sum for fp32 values (lane 63 ends with the wave's sum).
+__device__ inline float wave_incl_sum_f32(float x)
+{
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x111, 0xf, 0xf, false));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x112, 0xf, 0xf, false));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x114, 0xf, 0xf, false));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x118, 0xf, 0xf, false));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x142, 0xa, 0xf, false));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x143, 0xc, 0xf, false));
+    return x;
+}
+
 // As wave_incl_sum with max, for x >= 0.
 __device__ inline int wave_incl_max(int x)
 {
@@ -294,10 +306,8 @@ __device__ inline void new_token_logits(const AttnParams& p, const NewTokenRows<
 {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-        float x = fmaf((float)r.q2[h][0], (float)r.k2[0], (float)r.q2[h][1] * (float)r.k2[1]);
-#pragma unroll
-        for (int m = 32; m >= 1; m >>= 1) x += wave_shfl_xor(x, m);
-        if (lane == 0) s_new[h] = x * p.scale_log2;
+        const float x = wave_incl_sum_f32(fmaf((float)r.q2[h][0], (float)r.k2[0], (float)r.q2[h][1] * (float)r.k2[1]));
+        if (lane == 63) s_new[h] = x * p.scale_log2;
     }
 }
 
