@@ -146,3 +146,53 @@ def test_fused_append_on_the_checked_path(torch_cuda, apex, oracle_mod):
     assert apex.check_device_error() == 0
     check(out.cpu().numpy(), ref, "checked path")
     assert np.array_equal(kd.cpu().numpy().view(np.uint16), exp_k.view(np.uint16))
+
+
+@pytest.mark.parametrize("name", ["c2", "c4"])
+def test_fused_append_full_size_sampled(torch_cuda, apex, oracle_mod, name):
+    """The fused call at full size, in the benchmark's launch configuration
+    (default grid).  Oracle inputs are the picked requests' caches copied
+    before the call (current slots holding NaN), with the oracle's own append
+    of the new rows applied on the host; every request's slot is then checked
+    bit for bit on the device."""
+    torch = torch_cuda
+    print(f"[fused full-size] generating {name}", flush=True)
+    wl = W.DeviceWorkload(name)
+    cfg = wl.cfg
+    B, Hkv = cfg.B, cfg.Hkv
+    lens = np.asarray(wl.lens, dtype=np.int64)
+    blocks = np.asarray([wl.layout.block_table[b, (L - 1) // BS] for b, L in enumerate(lens)], dtype=np.int64)
+    pos = (lens - 1) % BS
+    dev = "cuda"
+    blk_d, pos_d = torch.from_numpy(blocks).to(dev), torch.from_numpy(pos).to(dev)
+    for c in (wl.k_cache, wl.v_cache):
+        c[blk_d, :, pos_d, :] = float("nan")
+    g = torch.Generator(device=dev)
+    g.manual_seed(77)
+    kn = torch.randn((B, Hkv, D), generator=g, device=dev).half()
+    vn = torch.randn((B, Hkv, D), generator=g, device=dev).half()
+
+    rng = np.random.default_rng(101)
+    picks = {int(np.argmax(lens)), int(np.argmin(lens)), 0, B - 1}
+    picks.update(int(x) for x in rng.choice(B, size=4, replace=False))
+    picks = sorted(picks)
+    case = wl.host_request_case(picks)            # before the call: NaN in the current slots
+    slots = np.asarray([int(case.block_table[i, (int(case.context_lens[i]) - 1) // BS]) * BS +
+                        (int(case.context_lens[i]) - 1) % BS for i in range(len(picks))], dtype=np.int64)
+    sel = torch.tensor(picks, device=dev)
+    exp_k, exp_v = kv_cache.kv_append(case.k_cache, case.v_cache, kn[sel].cpu().numpy(),
+                                      vn[sel].cpu().numpy(), slots)
+    ref = oracle_mod.decode_attention_f64(case.q, exp_k, exp_v, case.block_table, case.context_lens,
+                                          case.scale)
+
+    apex.decode_attention_ex(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens, wl.scale,
+                             out=wl.out, k_new=kn, v_new=vn)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(wl.out).all())
+    check(wl.out[sel].cpu().numpy(), ref, f"{name} fused, requests {picks}")
+    got_k = wl.k_cache[blk_d, :, pos_d, :]
+    got_v = wl.v_cache[blk_d, :, pos_d, :]
+    assert torch.equal(got_k.view(torch.int16), kn.view(torch.int16))
+    assert torch.equal(got_v.view(torch.int16), vn.view(torch.int16))
+    del wl
+    torch.cuda.empty_cache()
