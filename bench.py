@@ -37,6 +37,14 @@ JSON line:
              (one token per request at position L_b - 1 of the workload's
              cache) and a prompt-sized bulk append (65536 tokens) against the
              HBM peak; bytes = new K/V rows read + cache rows written + slots
+  fused_append  one layer-step as apex_kv_append + attention (two launches)
+             and as one fused call (k_new/v_new), back to back
+  scheduler  Alg. 2's decision for this GPU batch plus a host batch, from
+             the committed MI355X profile, and the cost of one decision
+  host       CPU model, sockets, NUMA nodes and usable cores of the host
+Inside roofline, kernel_us_cold_median / achieved_cold time the kernel after
+a 512 MiB read has evicted the caches (the figure that relies on no K/V left
+in a cache by the previous call).
 
 The default workload is the Llama-3.1-8B GQA long-output decode batch (B=32,
 32 q-heads over 8 kv-heads, d=128, block_size 16, context lengths lognormal
