@@ -384,3 +384,28 @@ def test_binding_tensor_check(case):
             A._require(t[:, ::2], "x", torch.float16, cpu)
         A._require(t[:, ::2], "x", torch.float16, cpu, contiguous=False)
     A._require(t, "x", torch.float16, cpu, shape=(4, 6))
+
+
+def test_partition_huge_unit_counts_divide_exactly(lib):
+    """Unit counts past 2^32 (the 32-bit division path no longer applies):
+    contributors per pair against exact integer arithmetic."""
+    lens = [2 ** 31 - 1, 5, 2 ** 30, 70000]
+    Hkv = 32
+    for launched in (1024, 7, 100000):
+        p = A.plan_host(lens, Hkv, launched)
+        blocks = [-(-L // 16) for L in lens]
+        U = sum(blocks) * Hkv
+        pairs = sum(1 for nb in blocks if nb > 0) * Hkv
+        W = min(launched, max(1, U // 8, pairs))
+        assert U > 2 ** 32 and p["units"] == U and p["active"] == W
+
+        def worker_of(u):
+            return ((u + 1) * W - 1) // U
+
+        pre = 0
+        for b, nb in enumerate(blocks):
+            for g in range(Hkv):
+                p0 = (pre * Hkv) + g * nb
+                want = worker_of(p0 + nb - 1) - worker_of(p0) + 1
+                assert p["contributors"][b, g] == want, (launched, b, g)
+            pre += nb
