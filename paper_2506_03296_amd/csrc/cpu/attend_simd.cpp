@@ -238,11 +238,13 @@ inline void pv_heads(const uint16_t* vr, int n, int d, const float* pw, int h0, 
     pv_block<HB, 1>(vr, n, d, pw, h0, acc, full, dc);
 }
 
-}  // namespace
-
-void attend(const Problem& p, int b, int g, int t0, int t1, State st, float* scratch)
+// attend() for GT heads of dimension DT (0 = the values in p): the common
+// shapes get compile-time trip counts, so the head and chunk loops unroll and
+// the heads' softmax chains can overlap.
+template <int GT, int DT>
+inline void attend_impl(const Problem& p, int b, int g, int t0, int t1, State st, float* scratch)
 {
-    const int G = p.G, d = p.d, dc = d / W;
+    const int G = GT > 0 ? GT : p.G, d = DT > 0 ? DT : p.d, dc = d / W;
     float* qs = scratch;                   // [G][d] query rows, pre-scaled
     float* pw = qs + (int64_t)G * d;       // [G][16] weights of the tile
     float* kt = pw + (int64_t)G * 16;      // [W][d] K tile widened to fp32 (partial tiles)
@@ -327,6 +329,22 @@ void attend(const Problem& p, int b, int g, int t0, int t1, State st, float* scr
         for (; h0 < G; ++h0) pv_heads<1>(vr, n, d, pw, h0, st.acc);
         t += n;
     }
+}
+
+}  // namespace
+
+void attend(const Problem& p, int b, int g, int t0, int t1, State st, float* scratch)
+{
+    if (p.d == 128) {
+        switch (p.G) {
+            case 1: return attend_impl<1, 128>(p, b, g, t0, t1, st, scratch);
+            case 2: return attend_impl<2, 128>(p, b, g, t0, t1, st, scratch);
+            case 4: return attend_impl<4, 128>(p, b, g, t0, t1, st, scratch);
+            case 8: return attend_impl<8, 128>(p, b, g, t0, t1, st, scratch);
+            default: break;
+        }
+    }
+    attend_impl<0, 0>(p, b, g, t0, t1, st, scratch);
 }
 
 void finish(const float* m, const float* l, const float* acc, int G, int d, uint16_t* out, float* lse)
