@@ -125,22 +125,28 @@ def test_single_submit_matches_oracles(torch_cuda, ov, oracle_mod, packed):
 
 def test_deferred_collection_over_iterations(torch_cuda, ov, oracle_mod):
     """Iteration n submits every layer, then collects iteration n-1's results
-    (one iteration late, as the overlap schedule does); three iterations."""
+    (one iteration late, as the overlap schedule does); three iterations.
+    The runtime appends to a layer's host cache while that layer has jobs
+    pending, so the expected caches are the test's own (the oracle's append
+    applied iteration by iteration); the runtime's caches are compared with
+    them once nothing is pending."""
     torch = torch_cuda
     layers = 3
     with make_runtime(ov, layers=layers) as rt:
         reqs = [Requests(torch, [30, 47, 5, 120], 96, seed=10 + l, packed=l % 2 == 1) for l in range(layers)]
+        model = []
         for l in range(layers):
-            reqs[l].fill(*rt.host_cache(l))
+            k, v = rt.host_cache(l)
+            reqs[l].fill(k, v)
+            model.append((k.copy(), v.copy()))
         prev = None
         for it in range(3):
             cur = []
             for l in range(layers):
-                k, v = rt.host_cache(l)
-                kb, vb = k.copy(), v.copy()
                 q, kn, vn = reqs[l].next_token()
                 t = rt.submit(l, q, kn, vn, reqs[l].slots, reqs[l].layout.block_table, reqs[l].lens)
-                ref, _, _ = reqs[l].expected(oracle_mod, kb, vb)
+                ref, kc, vc = reqs[l].expected(oracle_mod, *model[l])
+                model[l] = (kc, vc)
                 cur.append((t, ref, torch.empty_like(q)))
             if prev is not None:
                 for l, (t, ref, out) in enumerate(prev):
@@ -154,8 +160,12 @@ def test_deferred_collection_over_iterations(torch_cuda, ov, oracle_mod):
         for l, (t, ref, out) in enumerate(prev):
             rt.wait(t, out)
         torch.cuda.synchronize()
+        assert rt.pending() == 0
         for l, (t, ref, out) in enumerate(prev):
             assert_close(out.cpu().numpy(), ref, f"last iteration layer {l}")
+            k, v = rt.host_cache(l)
+            assert np.array_equal(k.view(np.uint16), model[l][0].view(np.uint16)), f"layer {l} K cache"
+            assert np.array_equal(v.view(np.uint16), model[l][1].view(np.uint16)), f"layer {l} V cache"
 
 
 def test_poll_does_not_block_while_held(torch_cuda, ov, oracle_mod):
