@@ -145,6 +145,27 @@ __device__ inline int wave_incl_max(int x)
     return x;
 }
 
+// Max / sum of the values a lane's column holds in the four 16-lane rows of
+// its wave (the rows' lanes l, l + 16, l + 32, l + 48), with the gfx950 row
+// swaps: each swap returns the lane's own value and its partner's (rows
+// paired as 0-1, 2-3, then halves as 0-32), so the pair's max / sum is the
+// step of a xor-16 / xor-32 butterfly without the LDS crossbar of a shuffle.
+__device__ inline float rows_max4(float x)
+{
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ inline float rows_sum4(float x)
+{
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ inline int uniform(int x)
 {
     return __builtin_amdgcn_readfirstlane(x);
@@ -438,9 +459,7 @@ __device__ inline void wave_attend(const AttnParams& p, const WaveSeg& cs, const
             for (int i = 0; i < 4; ++i)
                 if (tok0 + 4 * q + i >= L) sv[i] = -INFINITY;
         }
-        float bm = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-        bm = fmaxf(bm, wave_shfl_xor(bm, 16));
-        bm = fmaxf(bm, wave_shfl_xor(bm, 32));
+        const float bm = rows_max4(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])));
         const float mnew = fmaxf(m, bm);   // finite: the block holds a valid token
         const float alpha = exp2_fast(m - mnew);
         f32x4 pw;
@@ -497,8 +516,7 @@ __device__ inline void wave_attend(const AttnParams& p, const WaveSeg& cs, const
     st.prefetched = pf;
 
     // the wave's state for head h: l summed over the four token groups
-    float lw = l + wave_shfl_xor(l, 16);
-    lw += wave_shfl_xor(lw, 32);
+    const float lw = rows_sum4(l);
     if (col < G) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
