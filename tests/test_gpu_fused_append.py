@@ -196,3 +196,48 @@ def test_fused_append_full_size_sampled(torch_cuda, apex, oracle_mod, name):
     assert torch.equal(got_v.view(torch.int16), vn.view(torch.int16))
     del wl
     torch.cuda.empty_cache()
+
+
+def test_fused_append_checked_path_bad_current_block(torch_cuda, apex, oracle_mod):
+    """The checked path when the current token's own table entry is outside
+    the pool: the error bit is set and nothing is stored; that block's cached
+    tokens are skipped like any bad block, and the current token is still
+    attended from the new rows."""
+    torch = torch_cuda
+    lens = [40, 17]
+    G, Hkv = 4, 8
+    case = W.make_host_case(lens, G * Hkv, Hkv, seed=151, poison=True)
+    NB = case.k_cache.shape[0]
+    rng = np.random.default_rng(152)
+    kn = rng.standard_normal((2, Hkv, D)).astype(np.float16)
+    vn = rng.standard_normal((2, Hkv, D)).astype(np.float16)
+    bt = case.block_table.copy()
+    bt[0, 2] = NB + 7                                 # request 0's current block (tokens 32..39)
+    kc, vc = case.k_cache.copy(), case.v_cache.copy()
+    s1 = int(bt[1, 1]) * BS + 0                       # request 1's current slot (position 16)
+    kc[s1 // BS, :, s1 % BS, :] = np.float16(np.nan)
+    vc[s1 // BS, :, s1 % BS, :] = np.float16(np.nan)
+    exp_k, exp_v = kv_cache.kv_append(kc, vc, kn[1:], vn[1:], np.array([s1], dtype=np.int64))
+
+    # expected: request 0 over tokens 0..31 plus the current token, placed in
+    # an extra block at position 32; request 1 as usual
+    k_ext = np.concatenate([exp_k, np.full((1, Hkv, BS, D), np.nan, dtype=np.float16)])
+    v_ext = np.concatenate([exp_v, np.full((1, Hkv, BS, D), np.nan, dtype=np.float16)])
+    k_ext[NB, :, 0, :] = kn[0]
+    v_ext[NB, :, 0, :] = vn[0]
+    bt_ext = case.block_table.copy()
+    bt_ext[0, 2] = NB
+    ref = oracle_mod.decode_attention_f64(case.q, k_ext, v_ext, bt_ext, np.array([33, 17], dtype=np.int32),
+                                          case.scale)
+
+    dev = "cuda"
+    kd, vd = torch.from_numpy(kc).to(dev), torch.from_numpy(vc).to(dev)
+    out = apex.decode_attention_ex(torch.from_numpy(case.q).to(dev), kd, vd, torch.from_numpy(bt).to(dev),
+                                   torch.from_numpy(case.context_lens).to(dev), case.scale,
+                                   check_inputs=True, k_new=torch.from_numpy(kn).to(dev),
+                                   v_new=torch.from_numpy(vn).to(dev))
+    torch.cuda.synchronize()
+    assert apex.check_device_error() == apex.DEVICE_ERR_BLOCK_ID
+    check(out.cpu().numpy(), ref, "bad current block")
+    assert np.array_equal(kd.cpu().numpy().view(np.uint16), exp_k.view(np.uint16))
+    assert np.array_equal(vd.cpu().numpy().view(np.uint16), exp_v.view(np.uint16))
