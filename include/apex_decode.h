@@ -133,7 +133,9 @@ typedef struct apex_decode_args {
      * written to its slot -- the block_table entry of position L_b - 1, slot
      * (L_b - 1) % block_size -- during the call (no request may share that
      * slot).  Equivalent to apex_kv_append of these rows followed by the
-     * plain call, in one launch. */
+     * plain call, in one launch.  With APEX_DECODE_FLAG_CHECK_INPUTS, a
+     * current token whose table entry is outside the pool is attended but
+     * not stored (APEX_DEVICE_ERR_BLOCK_ID). */
     const void* k_new;
     const void* v_new;
     int64_t new_token_stride;
