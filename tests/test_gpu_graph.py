@@ -112,3 +112,56 @@ def test_layer_step_graph_replays_bitwise(torch_cuda, apex):
     torch.cuda.synchronize()
     assert np.array_equal(bits(out), bits(ref2)), "replay after changing q in place"
     assert not np.array_equal(bits(ref2), bits(ref))
+
+
+def test_fused_layer_step_graph_replays_bitwise(torch_cuda, apex):
+    """The fused call (attention + append of the current token in one
+    launch) with a caller workspace, captured and replayed: every replay
+    equals the eager fused call bit for bit, outputs and caches."""
+    torch = torch_cuda
+    lens = [300, 17, 1600, 64, 0, 999, 4096, 1]
+    case = W.make_host_case(lens, HQ, HKV, seed=99)
+    B = len(lens)
+    dev = "cuda"
+    rng = np.random.default_rng(100)
+    q = torch.from_numpy(case.q).to(dev)
+    bt = torch.from_numpy(case.block_table).to(dev)
+    cl = torch.from_numpy(case.context_lens).to(dev)
+    k_new = torch.from_numpy(rng.standard_normal((B, HKV, D)).astype(np.float16)).to(dev)
+    v_new = torch.from_numpy(rng.standard_normal((B, HKV, D)).astype(np.float16)).to(dev)
+
+    def eager():
+        kc = torch.from_numpy(case.k_cache).to(dev)
+        vc = torch.from_numpy(case.v_cache).to(dev)
+        out = apex.decode_attention_ex(q, kc, vc, bt, cl, case.scale, k_new=k_new, v_new=v_new)
+        torch.cuda.synchronize()
+        return out, kc, vc
+
+    ref, ref_k, ref_v = eager()
+    kc = torch.from_numpy(case.k_cache).to(dev)
+    vc = torch.from_numpy(case.v_cache).to(dev)
+    ws = torch.zeros(apex.workspace_bytes(B, HQ, HKV), dtype=torch.uint8, device=dev)
+    out = torch.empty_like(q)
+
+    def step():
+        apex.decode_attention_ex(q, kc, vc, bt, cl, case.scale, out=out, workspace=ws, k_new=k_new, v_new=v_new)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(out), bits(ref)), "eager fused call with the caller workspace"
+
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize()
+    for rep in range(4):
+        out.fill_(7.0)
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(bits(out), bits(ref)), f"replay {rep}"
+        assert np.array_equal(bits(kc), bits(ref_k)) and np.array_equal(bits(vc), bits(ref_v)), f"caches, replay {rep}"
+    assert int(ws[:apex.counter_bytes(B, HKV)].to(torch.int32).abs().sum()) == 0
