@@ -103,7 +103,7 @@ typedef struct apex_decode_args {
     /* work groups of the persistent launch; 0 = as many as the device keeps
      * resident.  The work (one unit = one 16-token block of one kv-head) is
      * cut into equal contiguous ranges, one per work group; with 0 a range is
-     * never shorter than 8 units unless that would leave fewer ranges than
+     * never shorter than 16 units unless that would leave fewer ranges than
      * non-empty (request, kv-head) pairs, and a batch of at most one pair per
      * CU (and at most 1024 units per CU) uses one work group per CU; with
      * n > 0 every range holds at least one unit (tests use this to force

@@ -23,7 +23,7 @@ namespace apex {
 
 constexpr int kHeadDim = 128;
 constexpr int kBlockSize = 16;
-constexpr int kMinUnitsPerWorker = 8;   // two blocks per wave of a 4-wave work group
+constexpr int kMinUnitsPerWorker = 16;  // four blocks per wave of a 4-wave work group
 constexpr int64_t kUnitsPerCuForOne = 1024;   // 8 MiB of K/V per CU
 
 // floor(a / b) for a >= 0, b > 0.  A 64-bit division is a long software

@@ -76,7 +76,7 @@ def _brute_partition(lens, Hkv, launched, forced, cus=0):
     pairs = sum(1 for nb in blocks if nb > 0) * Hkv
     if not forced and cus > 0 and pairs <= cus and U <= 1024 * cus:
         launched = min(launched, cus)
-    W = min(launched, max(1, U // (1 if forced else 8), pairs))
+    W = min(launched, max(1, U // (1 if forced else 16), pairs))
     owner = []
     starts = [w * U // W for w in range(W + 1)]
     for w in range(W):
@@ -396,7 +396,7 @@ def test_partition_huge_unit_counts_divide_exactly(lib):
         blocks = [-(-L // 16) for L in lens]
         U = sum(blocks) * Hkv
         pairs = sum(1 for nb in blocks if nb > 0) * Hkv
-        W = min(launched, max(1, U // 8, pairs))
+        W = min(launched, max(1, U // 16, pairs))
         assert U > 2 ** 32 and p["units"] == U and p["active"] == W
 
         def worker_of(u):
