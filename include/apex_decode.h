@@ -25,7 +25,12 @@
  *                device; entries past ceil(L_b / block_size) are never read
  *   context_lens int32 [B]; counts the current token (its K/V must already be
  *                in the cache); L_b <= 0 yields a zero output row
- *   out          fp16  [B][Hq][d]; must not overlap q
+ *   out          fp16  [B][Hq][d]; must not overlap any input.  Checked on
+ *                the host against q, context_lens, the new rows of the fused
+ *                append, and the extents of k_cache, v_cache and block_table
+ *                the call knows: num_blocks blocks when apex_decode_args
+ *                gives them (else the first block), B rows of an explicit
+ *                block_table_stride (else one entry per request)
  *
  * Supported: d = 128, block_size = 16, Hq % Hkv == 0 with Hq / Hkv in
  * {1, 2, 4, 8}.  Anything else returns APEX_ERR_UNSUPPORTED.
@@ -123,7 +128,9 @@ typedef struct apex_decode_args {
     void* attn_kernel_events[2];
     /* APEX_DECODE_FLAG_* bits; other bits must be 0 */
     uint32_t flags;
-    /* physical blocks in k_cache/v_cache; needed by APEX_DECODE_FLAG_CHECK_INPUTS */
+    /* physical blocks in k_cache/v_cache (0 = not given; negative is an
+     * error); needed by APEX_DECODE_FLAG_CHECK_INPUTS, and when given the
+     * overlap check of out covers the whole caches */
     int64_t num_blocks;
     /* Fused append (both NULL = off): the current token's K and V rows, fp16
      * [B][Hkv][d] with new_token_stride elements between tokens (0 = Hkv * d;
@@ -135,7 +142,11 @@ typedef struct apex_decode_args {
      * slot).  Equivalent to apex_kv_append of these rows followed by the
      * plain call, in one launch.  With APEX_DECODE_FLAG_CHECK_INPUTS, a
      * current token whose table entry is outside the pool is attended but
-     * not stored (APEX_DEVICE_ERR_BLOCK_ID). */
+     * not stored (APEX_DEVICE_ERR_BLOCK_ID); a context longer than its
+     * explicit table row keeps every cached token of the row, and its
+     * current token, whose position then lies past the row, is attended but
+     * not stored, so the row's last slot keeps its cached token
+     * (APEX_DEVICE_ERR_TABLE_ROW). */
     const void* k_new;
     const void* v_new;
     int64_t new_token_stride;

@@ -152,6 +152,19 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb)
     return x < y + nb && y < x + na;
 }
 
+// a * b, saturated at the largest size (an extent past the address space
+// still overlaps everything above its start)
+size_t sat_mul(size_t a, size_t b)
+{
+    return b != 0 && a > SIZE_MAX / b ? SIZE_MAX : a * b;
+}
+
+size_t sat_extent(const void* base, size_t bytes)
+{
+    const size_t room = SIZE_MAX - (uintptr_t)base;
+    return bytes < room ? bytes : room;
+}
+
 int check_shapes(int B, int Hq, int Hkv, int d, int block_size)
 {
     if (B < 0) return fail(APEX_ERR_INVALID_ARG, "B = %d is negative", B);
@@ -207,80 +220,16 @@ int dispatch(int G, bool check, bool append, const apex::AttnParams& p, const in
                   : dispatch_g<false, false>(G, p, bt, lens, workers, ev, stream);
 }
 
-}  // namespace
-
-extern "C" {
-
-int apex_decode_version(void) { return 310; }
-
-const char* apex_decode_last_error(void) { return apex::last_error_message(); }
-
-size_t apex_decode_counter_bytes(int B, int Hkv)
+// Validates a call and enqueues its kernel.  The arrival counters and the
+// partials come from the caller's workspace or the library-owned workspace of
+// the device.
+int enqueue(const apex_decode_args& a)
 {
-    if (B < 0 || Hkv <= 0) return 0;
-    return counter_bytes(B, Hkv);
-}
-
-size_t apex_decode_workspace_bytes(int B, int Hq, int Hkv, int d, int block_size, int num_workers)
-{
-    if (check_shapes(B, Hq, Hkv, d, block_size) != APEX_OK || num_workers < 0) return 0;
-    int64_t workers = num_workers;
-    if (workers == 0) {
-        int dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess || default_workers(dev, Hq / Hkv, &workers) != APEX_OK)
-            return 0;
-    }
-    return counter_bytes(B, Hkv) + partial_bytes(workers, Hq / Hkv);
-}
-
-int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block_size,
-                          int launched_workers, int forced, int cus, int32_t* contributors_out,
-                          int64_t* units_out, int64_t* active_out, int64_t* partials_out)
-{
-    apex::clear_error();
-    if (B < 0 || Hkv <= 0 || launched_workers <= 0 || cus < 0)
-        return fail(APEX_ERR_INVALID_ARG, "bad partition arguments");
-    if (B > 0 && !context_lens) return fail(APEX_ERR_INVALID_ARG, "context_lens is NULL");
-    if (block_size != apex::kBlockSize)
-        return fail(APEX_ERR_UNSUPPORTED, "block_size %d unsupported (only 16)", block_size);
-    int64_t blocks = 0, nonempty = 0;
-    for (int b = 0; b < B; ++b) {
-        blocks += apex::blocks_of(context_lens[b], block_size);
-        nonempty += context_lens[b] > 0;
-    }
-    const int64_t units = blocks * Hkv;
-    const int64_t W = apex::active_workers(units, launched_workers,
-                                           forced ? 1 : apex::kMinUnitsPerWorker, nonempty * Hkv,
-                                           forced ? 0 : cus);
-    int64_t partials = 0, pre = 0;
-    for (int b = 0; b < B; ++b) {
-        const int64_t nb = apex::blocks_of(context_lens[b], block_size);
-        for (int g = 0; g < Hkv; ++g) {
-            int64_t n = 0;
-            if (nb > 0) {
-                const int64_t p0 = pre * Hkv + (int64_t)g * nb;
-                n = apex::worker_of(p0 + nb - 1, units, W) - apex::worker_of(p0, units, W) + 1;
-                if (n > 1) partials += n;
-            }
-            if (contributors_out) contributors_out[(size_t)b * Hkv + g] = (int32_t)n;
-        }
-        pre += nb;
-    }
-    if (units_out) *units_out = units;
-    if (active_out) *active_out = units > 0 ? W : 0;
-    if (partials_out) *partials_out = partials;
-    return APEX_OK;
-}
-
-int apex_decode_attention_ex(const apex_decode_args* args)
-{
-    apex::clear_error();
-    if (!args) return fail(APEX_ERR_INVALID_ARG, "args is NULL");
-    const apex_decode_args& a = *args;
     int rc = check_shapes(a.B, a.Hq, a.Hkv, a.d, a.block_size);
     if (rc != APEX_OK) return rc;
     if (a.flags & ~APEX_DECODE_FLAG_CHECK_INPUTS) return fail(APEX_ERR_INVALID_ARG, "unknown flags");
     const bool check = (a.flags & APEX_DECODE_FLAG_CHECK_INPUTS) != 0;
+    if (a.num_blocks < 0) return fail(APEX_ERR_INVALID_ARG, "num_blocks is negative");
     if (check && a.num_blocks <= 0)
         return fail(APEX_ERR_INVALID_ARG, "the input check needs num_blocks > 0");
     if (a.num_workers < 0 || a.num_workers > kMaxWorkers)
@@ -311,6 +260,19 @@ int apex_decode_attention_ex(const apex_decode_args* args)
         return fail(APEX_ERR_INVALID_ARG, "out overlaps context_lens");
     if (a.lse_out && overlaps(a.lse_out, (size_t)a.B * a.Hq * 4, a.out, qo_bytes))
         return fail(APEX_ERR_INVALID_ARG, "lse_out overlaps out");
+    // the caches and the table over the extents the host knows: num_blocks
+    // blocks when given (else the first block), the rows of an explicit
+    // stride (else one entry per request)
+    const size_t block_bytes = (size_t)a.Hkv * a.block_size * a.d * 2;
+    const size_t cache_bytes = sat_mul(block_bytes, a.num_blocks > 0 ? (size_t)a.num_blocks : 1);
+    const size_t bt_bytes =
+        sat_mul((size_t)a.B * 4, a.block_table_stride > 0 ? (size_t)a.block_table_stride : 1);
+    if (overlaps(a.out, qo_bytes, a.k_cache, sat_extent(a.k_cache, cache_bytes)))
+        return fail(APEX_ERR_INVALID_ARG, "out overlaps k_cache");
+    if (overlaps(a.out, qo_bytes, a.v_cache, sat_extent(a.v_cache, cache_bytes)))
+        return fail(APEX_ERR_INVALID_ARG, "out overlaps v_cache");
+    if (overlaps(a.out, qo_bytes, a.block_table, sat_extent(a.block_table, bt_bytes)))
+        return fail(APEX_ERR_INVALID_ARG, "out overlaps block_table");
     if (append) {
         if (!aligned(a.k_new, 16) || !aligned(a.v_new, 16))
             return fail(APEX_ERR_INVALID_ARG, "k_new and v_new must be 16-byte aligned");
@@ -389,6 +351,78 @@ int apex_decode_attention_ex(const apex_decode_args* args)
     const int32_t* lens = a.context_lens;
     void* const* ev = a.attn_kernel_events;
     return dispatch(G, check, append, p, bt, lens, workers, ev, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+int apex_decode_version(void) { return 310; }
+
+const char* apex_decode_last_error(void) { return apex::last_error_message(); }
+
+size_t apex_decode_counter_bytes(int B, int Hkv)
+{
+    if (B < 0 || Hkv <= 0) return 0;
+    return counter_bytes(B, Hkv);
+}
+
+size_t apex_decode_workspace_bytes(int B, int Hq, int Hkv, int d, int block_size, int num_workers)
+{
+    if (check_shapes(B, Hq, Hkv, d, block_size) != APEX_OK || num_workers < 0) return 0;
+    int64_t workers = num_workers;
+    if (workers == 0) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess || default_workers(dev, Hq / Hkv, &workers) != APEX_OK)
+            return 0;
+    }
+    return counter_bytes(B, Hkv) + partial_bytes(workers, Hq / Hkv);
+}
+
+int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block_size,
+                          int launched_workers, int forced, int cus, int32_t* contributors_out,
+                          int64_t* units_out, int64_t* active_out, int64_t* partials_out)
+{
+    apex::clear_error();
+    if (B < 0 || Hkv <= 0 || launched_workers <= 0 || cus < 0)
+        return fail(APEX_ERR_INVALID_ARG, "bad partition arguments");
+    if (B > 0 && !context_lens) return fail(APEX_ERR_INVALID_ARG, "context_lens is NULL");
+    if (block_size != apex::kBlockSize)
+        return fail(APEX_ERR_UNSUPPORTED, "block_size %d unsupported (only 16)", block_size);
+    int64_t blocks = 0, nonempty = 0;
+    for (int b = 0; b < B; ++b) {
+        blocks += apex::blocks_of(context_lens[b], block_size);
+        nonempty += context_lens[b] > 0;
+    }
+    const int64_t units = blocks * Hkv;
+    const int64_t W = apex::active_workers(units, launched_workers,
+                                           forced ? 1 : apex::kMinUnitsPerWorker, nonempty * Hkv,
+                                           forced ? 0 : cus);
+    int64_t partials = 0, pre = 0;
+    for (int b = 0; b < B; ++b) {
+        const int64_t nb = apex::blocks_of(context_lens[b], block_size);
+        for (int g = 0; g < Hkv; ++g) {
+            int64_t n = 0;
+            if (nb > 0) {
+                const int64_t p0 = pre * Hkv + (int64_t)g * nb;
+                n = apex::worker_of(p0 + nb - 1, units, W) - apex::worker_of(p0, units, W) + 1;
+                if (n > 1) partials += n;
+            }
+            if (contributors_out) contributors_out[(size_t)b * Hkv + g] = (int32_t)n;
+        }
+        pre += nb;
+    }
+    if (units_out) *units_out = units;
+    if (active_out) *active_out = units > 0 ? W : 0;
+    if (partials_out) *partials_out = partials;
+    return APEX_OK;
+}
+
+int apex_decode_attention_ex(const apex_decode_args* args)
+{
+    apex::clear_error();
+    if (!args) return fail(APEX_ERR_INVALID_ARG, "args is NULL");
+    return enqueue(*args);
 }
 
 int apex_decode_attention(const void* q, const void* k_cache, const void* v_cache,

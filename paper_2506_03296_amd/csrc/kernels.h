@@ -555,11 +555,15 @@ __device__ inline void fold_new_token(float sn, float vn, float& M, float& num, 
 }
 
 // Writes element `dim` of the current token's K and V rows of kv-head g to
-// its cache slot: position Lc - 1 of request b (Lc = the full length).
+// its cache slot: position Lc - 1 of request b (Lc = the full length).  With
+// the input check, a position past an explicit table row (a context cut to
+// its row, already reported) is not stored: the row's last slot holds a
+// cached token.
 template <bool kCheck>
 __device__ inline void store_new_token(const AttnParams& p, const int32_t* bt_row, int b, int g, int Lc,
                                        int dim)
 {
+    if (kCheck && p.bt_stride > 0 && (int64_t)((Lc - 1) / kBlockSize) >= p.bt_stride) return;
     const int id = bt_row[(Lc - 1) / kBlockSize];
     if (kCheck && !(id >= 0 && (int64_t)id < p.num_blocks)) {
         if (dim == 0) report_error(p, kErrBlockId);
@@ -606,22 +610,27 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     // with the input check, a context longer than an explicit table row is
     // cut to the row (and reported)
     const int64_t row_tokens = p.bt_stride * kBlockSize;
-    auto clamp_len = [&](int L) -> int {
-        return kCheck && p.bt_stride > 0 && L > row_tokens ? (int)row_tokens : L;
-    };
-    // with the fused append the partition covers the cached tokens, the
-    // first L - 1; the tight table stride still follows the full lengths
+    auto is_cut = [&](int L) -> bool { return kCheck && p.bt_stride > 0 && L > row_tokens; };
+    // Tokens the partition covers: the cached ones.  With the fused append
+    // the current token (position L - 1) comes from the new rows, so the
+    // caches hold the first L - 1; a context cut to its row keeps every token
+    // of the row, and its current token, whose position lies past the row,
+    // is attended but has no slot to be stored in.  The tight table stride
+    // follows the (cut) full lengths.
     constexpr bool append = kAppend;
-    auto scan_len = [&](int Lc) -> int { return append && Lc > 0 ? Lc - 1 : Lc; };
+    auto cached_len = [&](int L) -> int {
+        if (is_cut(L)) return (int)row_tokens;
+        return append && L > 0 ? L - 1 : L;
+    };
     int tsum = 0, tmax = 0, tcnt = 0;
     for (int b = r0; b < r1; ++b) {
-        const int Lc = clamp_len(lens[b]);
-        if (kCheck && Lc != lens[b]) report_error(p, kErrTableRow);
-        const int L = scan_len(Lc);
+        const int raw = lens[b];
+        if (is_cut(raw)) report_error(p, kErrTableRow);
+        const int L = cached_len(raw);
         if (cached) s_lens[b] = L;
         const int nb = (int)blocks_of(L, kBlockSize);
         tsum += nb;
-        tmax = max(tmax, (int)blocks_of(Lc, kBlockSize));
+        tmax = max(tmax, (int)blocks_of(is_cut(raw) ? (int)row_tokens : raw, kBlockSize));
         tcnt += nb > 0;
     }
     int incl = wave_incl_sum(tsum);
@@ -641,7 +650,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         maxb = max(maxb, s_wmax[v]);
         nonempty += s_wcnt[v];
     }
-    auto len_of = [&](int b) -> int { return cached ? s_lens[b] : scan_len(clamp_len(lens[b])); };
+    auto len_of = [&](int b) -> int { return cached ? s_lens[b] : cached_len(lens[b]); };
 
     const int64_t units = (int64_t)uniform(total) * p.Hkv;
     const int64_t stride = p.bt_stride > 0 ? p.bt_stride : (int64_t)uniform(maxb);
@@ -842,7 +851,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     // (lse = its scaled logit) and stores its K/V
     for (int b = (int)w; b < B; b += (int)gridDim.x) {
         if (len_of(b) > 0) continue;
-        if (append && clamp_len(lens[b]) == 1) {
+        if (append && lens[b] == 1) {
             const size_t nrow = (size_t)b * p.new_stride;
             for (int i = tid; i < p.Hq * D; i += kAttnThreads) {
                 const int h = i / D, dim = i % D;

@@ -206,6 +206,11 @@ def call(lib, B=2, Hq=32, Hkv=8, d=128, bs=16, q=FAKE, k=FAKE + (1 << 30), v=FAK
     (dict(k=FAKE + (1 << 30) + 8), A.APEX_ERR_INVALID_ARG),
     (dict(bt=FAKE + (3 << 30) + 2), A.APEX_ERR_INVALID_ARG),
     (dict(out=FAKE + 64), A.APEX_ERR_INVALID_ARG),     # overlaps q
+    (dict(out=FAKE + (1 << 30)), A.APEX_ERR_INVALID_ARG),             # out = k_cache
+    (dict(out=FAKE + (2 << 30) + 4096), A.APEX_ERR_INVALID_ARG),      # inside v_cache's first block
+    (dict(out=FAKE + (1 << 30) - 4096), A.APEX_ERR_INVALID_ARG),      # runs into k_cache
+    (dict(out=FAKE + (3 << 30)), A.APEX_ERR_INVALID_ARG),             # out = block_table
+    (dict(out=FAKE + (4 << 30)), A.APEX_ERR_INVALID_ARG),             # out = context_lens
 ])
 def test_invalid_arguments_are_rejected(lib, kw, code):
     assert call(lib, **kw) == code
@@ -227,6 +232,28 @@ def test_ex_rejects_flags_and_negative_fields(lib):
         setattr(a, field, value)
         assert lib.apex_decode_attention_ex(ctypes.byref(a)) == A.APEX_ERR_INVALID_ARG
     assert lib.apex_decode_attention_ex(None) == A.APEX_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("field,where,needle", [
+    ("num_blocks", 1 << 20, "k_cache"),          # 1 MiB into a cache of 100 blocks (3.2 MB)
+    ("num_blocks", (1 << 30) + (3 << 20), "v_cache"),
+    ("block_table_stride", (2 << 30) + 640, "block_table"),   # row 1 of a 100-entry stride
+])
+def test_ex_out_overlap_over_the_known_extents(lib, field, where, needle):
+    """With num_blocks (or an explicit table stride) the whole caches (the
+    whole table) are checked against out, not just their start."""
+    a = _fake_args()
+    setattr(a, field, 100)
+    a.out = a.k_cache + where
+    assert lib.apex_decode_attention_ex(ctypes.byref(a)) == A.APEX_ERR_INVALID_ARG
+    assert needle in A.last_error()
+
+
+def test_ex_rejects_a_negative_block_count(lib):
+    a = _fake_args()
+    a.num_blocks = -1
+    assert lib.apex_decode_attention_ex(ctypes.byref(a)) == A.APEX_ERR_INVALID_ARG
+    assert "num_blocks" in A.last_error()
 
 
 def test_ex_check_flag_needs_the_block_count(lib):
@@ -409,3 +436,4 @@ def test_partition_huge_unit_counts_divide_exactly(lib):
                 want = worker_of(p0 + nb - 1) - worker_of(p0) + 1
                 assert p["contributors"][b, g] == want, (launched, b, g)
             pre += nb
+

@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 
 import apex_workloads as W
+import whole_tensor
 from oracle import kv_cache
 
 pytestmark = pytest.mark.gpu
@@ -148,13 +149,13 @@ def test_fused_append_on_the_checked_path(torch_cuda, apex, oracle_mod):
     assert np.array_equal(kd.cpu().numpy().view(np.uint16), exp_k.view(np.uint16))
 
 
-@pytest.mark.parametrize("name", ["c2", "c4"])
-def test_fused_append_full_size_sampled(torch_cuda, apex, oracle_mod, name):
+@pytest.mark.parametrize("name", ["c2", "c3", "c4", "c5"])
+def test_fused_append_full_size_whole_tensor(torch_cuda, apex, oracle_mod, name):
     """The fused call at full size, in the benchmark's launch configuration
-    (default grid).  Oracle inputs are the picked requests' caches copied
-    before the call (current slots holding NaN), with the oracle's own append
-    of the new rows applied on the host; every request's slot is then checked
-    bit for bit on the device."""
+    (default grid), over every request.  The oracle's inputs are each chunk of
+    requests copied before the call (current slots holding NaN) with the
+    oracle's own append of the new rows applied on the host; every request's
+    slot is then checked bit for bit on the device."""
     torch = torch_cuda
     print(f"[fused full-size] generating {name}", flush=True)
     wl = W.DeviceWorkload(name)
@@ -171,25 +172,22 @@ def test_fused_append_full_size_sampled(torch_cuda, apex, oracle_mod, name):
     g.manual_seed(77)
     kn = torch.randn((B, Hkv, D), generator=g, device=dev).half()
     vn = torch.randn((B, Hkv, D), generator=g, device=dev).half()
+    kn_h, vn_h = kn.cpu().numpy(), vn.cpu().numpy()
 
-    rng = np.random.default_rng(101)
-    picks = {int(np.argmax(lens)), int(np.argmin(lens)), 0, B - 1}
-    picks.update(int(x) for x in rng.choice(B, size=4, replace=False))
-    picks = sorted(picks)
-    case = wl.host_request_case(picks)            # before the call: NaN in the current slots
-    slots = np.asarray([int(case.block_table[i, (int(case.context_lens[i]) - 1) // BS]) * BS +
-                        (int(case.context_lens[i]) - 1) % BS for i in range(len(picks))], dtype=np.int64)
-    sel = torch.tensor(picks, device=dev)
-    exp_k, exp_v = kv_cache.kv_append(case.k_cache, case.v_cache, kn[sel].cpu().numpy(),
-                                      vn[sel].cpu().numpy(), slots)
-    ref = oracle_mod.decode_attention_f64(case.q, exp_k, exp_v, case.block_table, case.context_lens,
-                                          case.scale)
+    def append_on_host(case, reqs):
+        L = case.context_lens.astype(np.int64)
+        rows = np.arange(len(reqs))
+        slots = case.block_table[rows, (L - 1) // BS].astype(np.int64) * BS + (L - 1) % BS
+        exp_k, exp_v = kv_cache.kv_append(case.k_cache, case.v_cache, kn_h[reqs], vn_h[reqs], slots)
+        return W.HostCase(case.q, exp_k, exp_v, case.block_table, case.context_lens, case.scale)
 
+    print(f"[fused full-size] {name}: oracle over {B} requests", flush=True)
+    ref = whole_tensor.oracle_reference(oracle_mod, wl, prepare=append_on_host)
+    print(f"[fused full-size] {name}: GPU call", flush=True)
     apex.decode_attention_ex(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens, wl.scale,
                              out=wl.out, k_new=kn, v_new=vn)
     torch.cuda.synchronize()
-    assert bool(torch.isfinite(wl.out).all())
-    check(wl.out[sel].cpu().numpy(), ref, f"{name} fused, requests {picks}")
+    whole_tensor.assert_whole_tensor(wl.out.cpu().numpy(), ref, f"{name} fused")
     got_k = wl.k_cache[blk_d, :, pos_d, :]
     got_v = wl.v_cache[blk_d, :, pos_d, :]
     assert torch.equal(got_k.view(torch.int16), kn.view(torch.int16))
@@ -241,3 +239,56 @@ def test_fused_append_checked_path_bad_current_block(torch_cuda, apex, oracle_mo
     check(out.cpu().numpy(), ref, "bad current block")
     assert np.array_equal(kd.cpu().numpy().view(np.uint16), exp_k.view(np.uint16))
     assert np.array_equal(vd.cpu().numpy().view(np.uint16), exp_v.view(np.uint16))
+
+
+@pytest.mark.parametrize("workers", [0, 1, 3])
+def test_fused_append_checked_path_context_past_its_row(torch_cuda, apex, oracle_mod, workers):
+    """The checked path when a context is longer than its explicit table row:
+    the context is cut to the row's tokens, all of them cached, and the
+    current token, whose position lies past the row, is attended from the new
+    rows but not stored -- the row's last slot keeps its cached token."""
+    torch = torch_cuda
+    G, Hkv, stride = 4, 8, 4                          # rows of 4 blocks = 64 tokens
+    lens = [40, 64, 17]
+    case = W.make_host_case(lens, G * Hkv, Hkv, seed=161, poison=True, stride=stride)
+    NB = case.k_cache.shape[0]
+    rng = np.random.default_rng(162)
+    B = len(lens)
+    kn = rng.standard_normal((B, Hkv, D)).astype(np.float16)
+    vn = rng.standard_normal((B, Hkv, D)).astype(np.float16)
+    call_lens = np.array([41, 100, 18], dtype=np.int32)   # request 1: 100 > 64, cut to its row
+    kc, vc = case.k_cache.copy(), case.v_cache.copy()
+    slots = np.array([int(case.block_table[0, 40 // BS]) * BS + 40 % BS, -1,
+                      int(case.block_table[2, 17 // BS]) * BS + 17 % BS], dtype=np.int64)
+    for s in slots[slots >= 0]:
+        kc[s // BS, :, s % BS, :] = np.float16(np.nan)
+        vc[s // BS, :, s % BS, :] = np.float16(np.nan)
+    exp_k, exp_v = kv_cache.kv_append(kc, vc, kn, vn, slots)   # request 1 stores nothing
+
+    # expected: requests 0 and 2 as usual; request 1 over its 64 cached tokens
+    # plus the current token, placed in an extra block at position 64
+    k_ext = np.concatenate([exp_k, np.full((1, Hkv, BS, D), np.nan, dtype=np.float16)])
+    v_ext = np.concatenate([exp_v, np.full((1, Hkv, BS, D), np.nan, dtype=np.float16)])
+    k_ext[NB, :, 0, :] = kn[1]
+    v_ext[NB, :, 0, :] = vn[1]
+    bt_ext = np.concatenate([case.block_table, np.zeros((B, 1), dtype=np.int32)], axis=1)
+    bt_ext[1, 4] = NB
+    ref = oracle_mod.decode_attention_f64(case.q, k_ext, v_ext, bt_ext,
+                                          np.array([41, 65, 18], dtype=np.int32), case.scale)
+
+    dev = "cuda"
+    kd, vd = torch.from_numpy(kc).to(dev), torch.from_numpy(vc).to(dev)
+    assert apex.check_device_error() == 0
+    out = apex.decode_attention_ex(torch.from_numpy(case.q).to(dev), kd, vd,
+                                   torch.from_numpy(case.block_table).to(dev),
+                                   torch.from_numpy(call_lens).to(dev), case.scale,
+                                   block_table_stride=stride, num_workers=workers, check_inputs=True,
+                                   k_new=torch.from_numpy(kn).to(dev), v_new=torch.from_numpy(vn).to(dev))
+    torch.cuda.synchronize()
+    assert apex.check_device_error() == apex.DEVICE_ERR_TABLE_ROW
+    check(out.cpu().numpy(), ref, f"context past its row, workers={workers}")
+    got_k, got_v = kd.cpu().numpy(), vd.cpu().numpy()
+    last = int(case.block_table[1, 3])                # the row's last slot (position 63)
+    assert np.array_equal(got_k[last, :, 15].view(np.uint16), kc[last, :, 15].view(np.uint16))
+    assert np.array_equal(got_k.view(np.uint16), exp_k.view(np.uint16))
+    assert np.array_equal(got_v.view(np.uint16), exp_v.view(np.uint16))

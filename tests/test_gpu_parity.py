@@ -3,13 +3,14 @@
 Bar (fp16 outputs, fp32 accumulation): every output finite, max-abs error
 <= 2e-3 and relative L2 error <= 1e-3 against the unrounded fp64 oracle.
 Small cases are compared element by element; the full-size workloads run in
-the launch configuration the benchmark times and are compared on sampled
-requests (the oracle computes those requests one by one).
+the launch configuration the benchmark times and are compared over the whole
+output tensor (the oracle runs over every request, chunk by chunk).
 """
 import numpy as np
 import pytest
 
 import apex_workloads as W
+import whole_tensor
 
 pytestmark = pytest.mark.gpu
 
@@ -257,29 +258,24 @@ def test_repeated_runs_are_bitwise_identical(torch_cuda, apex):
 
 
 # ---------------------------------------------------------------------------
-# full-size workloads, sampled requests, in the benchmark's launch configuration
+# full-size workloads, every request, in the benchmark's launch configuration
 # ---------------------------------------------------------------------------
 
 @pytest.mark.parametrize("name", ["c2", "c3", "c4", "c5"])
-def test_full_size_sampled_parity(torch_cuda, apex, oracle_mod, name):
+def test_full_size_whole_tensor_parity(torch_cuda, apex, oracle_mod, name):
+    """The call the benchmark times (default grid, library workspace) over the
+    whole workload, against the fp64 oracle over every request: max-abs and
+    relative L2 over the whole [B][Hq][d] output."""
     torch = torch_cuda
     print(f"[full-size] generating {name}", flush=True)
     wl = W.DeviceWorkload(name)
+    print(f"[full-size] {name}: oracle over {wl.cfg.B} requests", flush=True)
+    ref = whole_tensor.oracle_reference(oracle_mod, wl)
+    print(f"[full-size] {name}: GPU call", flush=True)
     apex.decode_attention(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens,
                           wl.scale, out=wl.out)
     torch.cuda.synchronize()
-    out = wl.out.float()
-    assert bool(torch.isfinite(out).all())
-    lens = wl.lens
-    rng = np.random.default_rng(100)
-    picks = {int(np.argmax(lens)), int(np.argmin(lens)), 0, len(lens) - 1}
-    picks.update(int(x) for x in rng.choice(len(lens), size=4, replace=False))
-    picks = sorted(picks)
-    case = wl.host_request_case(picks)
-    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
-                                          case.context_lens, case.scale)
-    got = out[torch.tensor(picks, device="cuda")].cpu().numpy()
-    assert_parity(got, ref, f"{name} requests {picks}")
+    whole_tensor.assert_whole_tensor(wl.out.cpu().numpy(), ref, name)
     del wl
     torch.cuda.empty_cache()
 
