@@ -42,6 +42,15 @@ JSON line:
   scheduler  Alg. 2's decision for this GPU batch plus a host batch, from
              the committed MI355X profile, and the cost of one decision
   host       CPU model, sockets, NUMA nodes and usable cores of the host
+  parity     the output of the last timed step against the fp64 oracle over
+             the cpu_baseline sample (the whole batch of the default
+             workload): max-abs, relative L2, finite, against the attention
+             bar; the run exits non-zero after printing when it fails
+  workloads  every named workload (c1-c5) timed like the headline one:
+             whole step, kernel alone (events) and kernel with cold caches,
+             algorithmic GB/s and fraction of the HBM peak, and the committed
+             counter traffic when it matches the kernel source (c1, 13 MB,
+             fits in the caches: a latency figure)
 Inside roofline, kernel_us_cold_median / achieved_cold time the kernel after
 a 512 MiB read has evicted the caches (the figure that relies on no K/V left
 in a cache by the previous call).
@@ -65,6 +74,9 @@ if ROOT not in sys.path:
 METRIC = "decode-attn µs/layer-step + achieved HBM GB/s (% peak), Llama-3.1-8B GQA"
 PEAK_HBM_GBS = 8000.0
 COLD_REPS = 20        # calls timed after evicting the caches
+PARITY_MAX_ABS = 2e-3  # the attention bar: fp16 output, fp32 accumulation
+PARITY_REL_L2 = 1e-3
+WORKLOADS = ("c1", "c2", "c3", "c4", "c5")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
 # the files that define the attention kernel and its work partition: counter
 # summaries stay valid while their code (comments aside) is unchanged
@@ -107,8 +119,13 @@ def committed_traffic(workload):
     return entry.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(wl, target_s):
-    """Time the fp64 oracle on the host over the first requests of the batch."""
+def cpu_baseline(wl, target_s, timed_out=None):
+    """Time the fp64 oracle on the host over the first requests of the batch.
+
+    With ``timed_out`` (host copy of the output of the last timed step) the
+    oracle's result over those requests is also compared with it: the parity
+    of what the benchmark timed, against the attention bar (max-abs <= 2e-3,
+    relative L2 <= 1e-3, all finite)."""
     import numpy as np
 
     import oracle
@@ -119,18 +136,18 @@ def cpu_baseline(wl, target_s):
     def run(n):
         case = wl.host_request_case(range(n))
         t0 = time.perf_counter()
-        oracle.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
-                                    case.context_lens, case.scale, num_threads=threads)
-        return time.perf_counter() - t0, case
+        ref = oracle.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale, num_threads=threads)
+        return time.perf_counter() - t0, case, ref
 
     n = 1
-    dt, case = run(n)
+    dt, case, ref = run(n)
     if dt < target_s:
         per = dt / n
         n = int(min(cfg.B, max(1, target_s / max(per, 1e-6))))
-        dt, case = run(n)
+        dt, case, ref = run(n)
     nbytes = W.algorithmic_bytes(case.context_lens, n, cfg.Hq, cfg.Hkv, cfg.d)
-    return {
+    baseline = {
         "value": round(nbytes / dt / 1e9, 4),
         "unit": "GB/s",
         "cores": threads,
@@ -138,6 +155,22 @@ def cpu_baseline(wl, target_s):
         "sample": f"first {n} of {cfg.B} requests ({int(np.sum(case.context_lens))} tokens, "
                   f"{nbytes / 1e6:.1f} MB algorithmic), fp64 plain-loop oracle, {dt:.2f} s",
     }
+    parity = None
+    if timed_out is not None:
+        got = np.asarray(timed_out[:n], dtype=np.float64)
+        err = got - ref
+        max_abs = float(np.max(np.abs(err)))
+        rel = float(np.linalg.norm(err) / np.linalg.norm(ref))
+        finite = bool(np.all(np.isfinite(got)))
+        parity = {
+            "against": "fp64 oracle (the cpu_baseline sample)",
+            "output": "out of the last timed step",
+            "requests": n, "of": cfg.B,
+            "max_abs": max_abs, "rel_l2": rel, "finite": finite,
+            "bar": {"max_abs": PARITY_MAX_ABS, "rel_l2": PARITY_REL_L2},
+            "ok": finite and max_abs <= PARITY_MAX_ABS and rel <= PARITY_REL_L2,
+        }
+    return baseline, parity
 
 
 def host_info():
@@ -451,6 +484,106 @@ def measure_fused_step(A, torch, wl, steps=50, warmup=20):
                       "before and one after the fused run"}
 
 
+def time_workload(A, torch, wl, steps, warmup, workers=0):
+    """The timings of one workload: W untimed steps, K steps back to back
+    between two synchronisations (whole step), K steps with events recorded by
+    the library around the kernel (kernel alone), and COLD_REPS calls each
+    after a 512 MiB read (cold caches).  Returns the figures and a host copy
+    of the output of the last back-to-back step."""
+    def step(events=None):
+        A.decode_attention_ex(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens,
+                              wl.scale, out=wl.out, num_workers=workers, events=events)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # whole steps, back to back, no per-kernel events
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = start.elapsed_time(stop) / steps
+    timed_out = wl.out.cpu().numpy()
+
+    # the attention kernel alone: events recorded by the library around it,
+    # on the launch stream
+    ev_pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for _ in range(steps)]
+    for i in range(steps):
+        step(ev_pairs[i])
+    torch.cuda.synchronize()
+    kern_ms = sorted(a.elapsed_time(b) for a, b in ev_pairs)
+
+    # the same kernel with cold caches: before each call a 512 MiB read
+    # (outside the events) evicts the 256 MB Infinity Cache and the L2s with
+    # clean lines, so no K/V byte comes from a cache filled by the previous
+    # call and no write-back competes with the kernel
+    scratch = torch.ones(128 << 20, dtype=torch.int32, device="cuda")
+    cold_pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(COLD_REPS)]
+    torch.cuda.synchronize()
+    for pair in cold_pairs:
+        torch.amax(scratch)
+        step(pair)
+    torch.cuda.synchronize()
+    cold_ms = sorted(a.elapsed_time(b) for a, b in cold_pairs)
+    del scratch
+    return {"ms_per_step": ms_per_step, "wall_s_per_step": wall / steps, "kern_ms": kern_ms,
+            "cold_ms": cold_ms}, timed_out
+
+
+def workload_line(wl, t, traffic):
+    """One workload's figures: whole step and kernel alone, algorithmic GB/s
+    and their fraction of the 8 TB/s HBM peak."""
+    nbytes = wl.algorithmic_bytes
+    kern = sum(t["kern_ms"]) / len(t["kern_ms"])
+    cold = t["cold_ms"][len(t["cold_ms"]) // 2]
+    step_gbs = nbytes / (t["ms_per_step"] * 1e-3) / 1e9
+    kern_gbs = nbytes / (kern * 1e-3) / 1e9
+    cfg = wl.cfg
+    return {
+        "workload": cfg.title,
+        "B": cfg.B, "Hq": cfg.Hq, "Hkv": cfg.Hkv,
+        "total_tokens": int(wl.lens.sum()), "algorithmic_bytes": int(nbytes),
+        "us_per_layer_step": round(t["ms_per_step"] * 1e3, 2),
+        "step_GBps": round(step_gbs, 2),
+        "step_frac": round(step_gbs / PEAK_HBM_GBS, 4),
+        "kernel_us_mean": round(kern * 1e3, 2),
+        "kernel_GBps": round(kern_gbs, 2),
+        "kernel_frac": round(kern_gbs / PEAK_HBM_GBS, 4),
+        "kernel_us_cold_median": round(cold * 1e3, 2),
+        "kernel_frac_cold": round(nbytes / (cold * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "traffic": traffic,
+    }
+
+
+def measure_workloads(A, torch, W, names, steps, warmup, workers, done):
+    """The other named workloads, each generated, timed like the headline one
+    and freed in turn (``done`` holds lines already measured)."""
+    lines = dict(done)
+    for name in names:
+        if name in lines:
+            continue
+        log(f"workload {name}: generating")
+        wl = W.DeviceWorkload(name)
+        torch.cuda.synchronize()
+        t, _ = time_workload(A, torch, wl, steps, warmup, workers)
+        lines[name] = workload_line(wl, t, committed_traffic(name))
+        if name == "c1":
+            lines[name]["kind"] = "latency (13 MB: the batch fits in the caches)"
+        log(f"workload {name}: {lines[name]['us_per_layer_step']} us/step, "
+            f"kernel {lines[name]['kernel_us_mean']} us ({100 * lines[name]['kernel_frac']:.1f} %)")
+        del wl
+        torch.cuda.empty_cache()
+    return {k: lines[k] for k in names if k in lines}
+
+
 def _timed(fn):
     t0 = time.perf_counter()
     fn()
@@ -479,6 +612,8 @@ def main():
     ap.add_argument("--no-cpu-attention", action="store_true",
                     help="skip the host backend line")
     ap.add_argument("--no-overlap", action="store_true", help="skip the overlap runtime line")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the per-workload lines (c1-c5 timed like the headline one)")
     ap.add_argument("--overlap-sweep", action="store_true",
                     help="only run the overlap measurement over host-attended batch sizes")
     args = ap.parse_args()
@@ -529,55 +664,13 @@ def main():
     nbytes = wl.algorithmic_bytes
     torch.cuda.synchronize()
 
-    def step(events=None):
-        A.decode_attention_ex(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens,
-                              wl.scale, out=wl.out, num_workers=args.workers,
-                              events=events)
-
-    log(f"warmup {args.warmup}")
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    # whole steps, back to back, no per-kernel events
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    log(f"timing {args.steps} steps")
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    start.record()
-    for _ in range(args.steps):
-        step()
-    stop.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_per_step = start.elapsed_time(stop) / args.steps
-
-    # the attention kernel alone: events recorded by the library around it
-    ev_pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                for _ in range(args.steps)]
-    for i in range(args.steps):
-        step(ev_pairs[i])
-    torch.cuda.synchronize()
-    kern_ms = sorted(a.elapsed_time(b) for a, b in ev_pairs)
+    log(f"warmup {args.warmup}, timing {args.steps} steps")
+    t, timed_out = time_workload(A, torch, wl, args.steps, args.warmup, args.workers)
+    ms_per_step = t["ms_per_step"]
+    kern_ms = t["kern_ms"]
     kern_mean = sum(kern_ms) / len(kern_ms)
-
-    # the same kernel with cold caches: before each call a 512 MiB read
-    # (outside the events) evicts the 256 MB Infinity Cache and the L2s with
-    # clean lines, so no K/V byte comes from a cache filled by the previous
-    # call and no write-back competes with the kernel
-    scratch = torch.ones(128 << 20, dtype=torch.int32, device="cuda")
-    cold_pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                  for _ in range(COLD_REPS)]
-    torch.cuda.synchronize()
-    for pair in cold_pairs:
-        torch.amax(scratch)
-        step(pair)
-    torch.cuda.synchronize()
-    cold_ms = sorted(a.elapsed_time(b) for a, b in cold_pairs)
-    cold_med = cold_ms[len(cold_ms) // 2]
-    del scratch
-    log(f"{ms_per_step * 1e3:.1f} us/step (wall {wall * 1e6 / args.steps:.1f} us), "
+    cold_med = t["cold_ms"][len(t["cold_ms"]) // 2]
+    log(f"{ms_per_step * 1e3:.1f} us/step (wall {t['wall_s_per_step'] * 1e6:.1f} us), "
         f"attention kernel mean {kern_mean * 1e3:.1f} us")
 
     achieved = nbytes / (kern_mean * 1e-3) / 1e9
@@ -619,7 +712,9 @@ def main():
             "achieved_cold": round(nbytes / (cold_med * 1e-3) / 1e9, 2),
         },
         "cpu_baseline": None,
+        "parity": None,
     }
+    headline_line = workload_line(wl, t, traffic)
     if not args.no_cpu_attention:
         log("timing the host backend")
         threads = max(1, min(16, len(os.sched_getaffinity(0))))
@@ -635,11 +730,22 @@ def main():
         log("timing kv_append")
         result["kv_append"] = measure_append(A, torch, W, wl, max(10, args.steps))
     if not args.no_cpu_baseline:
-        log("timing the CPU oracle")
-        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        log("timing the CPU oracle (and checking the timed output against it)")
+        result["cpu_baseline"], result["parity"] = cpu_baseline(wl, args.cpu_seconds, timed_out)
+        p = result["parity"]
+        log(f"parity of the timed output over {p['requests']} requests: max_abs {p['max_abs']:.3e}, "
+            f"rel_l2 {p['rel_l2']:.3e} -> {'ok' if p['ok'] else 'FAILED'}")
     if not (args.no_cpu_baseline and args.no_cpu_attention and args.no_overlap):
         result["host"] = host_info()
+    if not args.no_workloads:
+        del wl
+        torch.cuda.empty_cache()
+        result["workloads"] = measure_workloads(A, torch, W, WORKLOADS, args.steps, args.warmup,
+                                                args.workers, {args.workload: headline_line})
     print(json.dumps(result), flush=True)
+    if result["parity"] is not None and not result["parity"]["ok"]:
+        print("bench.py: the timed output fails the parity bar against the oracle", file=sys.stderr)
+        sys.exit(1)
 
 
 if __name__ == "__main__":
