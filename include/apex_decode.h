@@ -165,6 +165,31 @@ typedef struct apex_decode_args {
 
 int apex_decode_attention_ex(const apex_decode_args* args);
 
+/*
+ * No-allocation variant of apex_decode_attention, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments and, on a device whose
+ * default grid fits the scratch below (MI355X: 512 work groups), the same
+ * launch and the same result bit for bit.  The arrival counters and the
+ * partial results live in a static device array of the library instead of a
+ * workspace: 4.3 MiB on every device that loads the library, held until the
+ * process ends.  The call allocates nothing (no hipMalloc, no hipFree, no
+ * allocating library routine).
+ *   Limits: B * Hkv <= 65536 (request, kv-head) pairs, else
+ *   APEX_ERR_UNSUPPORTED and nothing is enqueued; the launch uses at most
+ *   4096 / (Hq / Hkv) work groups.
+ *   The first call on a device looks the array up and clears its counters
+ *   with a kernel on `stream`; every launch leaves them zero.
+ *   Every call on a device shares that device's array: calls that overlap on
+ *   one device (streams with no ordering between them) race and give wrong
+ *   results.  Order them on one stream, or use apex_decode_attention_ex with
+ *   a workspace per stream.
+ */
+int apex_decode_attention_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                                  const int32_t* block_table, const int32_t* context_lens, void* out,
+                                  int B, int Hq, int Hkv, int d, int block_size, float scale,
+                                  void* stream);
+
 /* Workspace bytes a call with these shapes needs on the current device
  * (num_workers as in apex_decode_args).  0 on bad shapes. */
 size_t apex_decode_workspace_bytes(int B, int Hq, int Hkv, int d, int block_size, int num_workers);

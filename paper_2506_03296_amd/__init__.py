@@ -20,7 +20,7 @@ __all__ = [
     "workspace_bytes", "plan_host", "last_error", "release_workspace", "version",
     "APEX_OK", "APEX_ERR_INVALID_ARG", "APEX_ERR_UNSUPPORTED", "APEX_ERR_OUT_OF_MEMORY",
     "APEX_ERR_HIP", "EXPORTED_SYMBOLS", "counter_bytes", "kv_append", "check_device_error",
-    "FLAG_CHECK_INPUTS", "DEVICE_ERR_BLOCK_ID", "DEVICE_ERR_TABLE_ROW",
+    "FLAG_CHECK_INPUTS", "DEVICE_ERR_BLOCK_ID", "DEVICE_ERR_TABLE_ROW", "decode_attention_noalloc",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libapex_decode.so")
@@ -35,7 +35,7 @@ EXPORTED_SYMBOLS = (
     "apex_decode_attention", "apex_decode_attention_ex", "apex_decode_workspace_bytes",
     "apex_decode_counter_bytes", "apex_decode_plan_host", "apex_decode_last_error",
     "apex_decode_release_workspace", "apex_decode_version", "apex_kv_append",
-    "apex_decode_check_device_error",
+    "apex_decode_check_device_error", "apex_decode_attention_noalloc",
 )
 FLAG_CHECK_INPUTS = 1
 DEVICE_ERR_BLOCK_ID = 1
@@ -88,6 +88,8 @@ def load_library(path=None):
     lib.apex_decode_attention.restype = i32
     lib.apex_decode_attention.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32,
                                           ctypes.c_float, vp]
+    lib.apex_decode_attention_noalloc.restype = i32
+    lib.apex_decode_attention_noalloc.argtypes = lib.apex_decode_attention.argtypes
     lib.apex_decode_attention_ex.restype = i32
     lib.apex_decode_attention_ex.argtypes = [ctypes.POINTER(DecodeArgs)]
     lib.apex_decode_workspace_bytes.restype = ctypes.c_size_t
@@ -214,6 +216,22 @@ def decode_attention(q, k_cache, v_cache, block_table, context_lens, scale, out=
     rc = lib.apex_decode_attention(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
                                    _ptr(context_lens), _ptr(out), B, Hq, Hkv, d, bs,
                                    ctypes.c_float(scale), _stream_handle(stream, q.device))
+    _check(rc)
+    return out
+
+
+def decode_attention_noalloc(q, k_cache, v_cache, block_table, context_lens, scale, out,
+                             stream=None):
+    """apex_decode_attention_noalloc over torch tensors (the library
+    allocates nothing; ``out`` is the caller's); returns ``out``.  The block
+    table must be tight, as for ``decode_attention``."""
+    if out is None:
+        raise ValueError("decode_attention_noalloc writes into the caller's out")
+    B, Hq, Hkv, d, bs = _check_tensors(q, k_cache, v_cache, block_table, context_lens, out)
+    lib = load_library()
+    rc = lib.apex_decode_attention_noalloc(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                                           _ptr(context_lens), _ptr(out), B, Hq, Hkv, d, bs,
+                                           ctypes.c_float(scale), _stream_handle(stream, q.device))
     _check(rc)
     return out
 

@@ -40,6 +40,26 @@ const char* last_error_message() { return g_last_error; }
 
 namespace {
 
+// Static scratch of apex_decode_attention_noalloc: arrival counters for up to
+// kScratchPairs (request, kv-head) pairs, then the partial accumulators and
+// (max, sum) pairs of up to kScratchWorkerHeads (work group, q-head) pairs,
+// two slots each -- the layout of a workspace of that size, at fixed offsets.
+constexpr int64_t kScratchPairs = 1 << 16;
+constexpr int64_t kScratchWorkerHeads = 4096;
+constexpr size_t kScratchCounterBytes = kScratchPairs * sizeof(int32_t);
+constexpr size_t kScratchAccBytes = 2 * kScratchWorkerHeads * apex::kHeadDim * sizeof(float);
+constexpr size_t kScratchMlBytes = 2 * kScratchWorkerHeads * 2 * sizeof(float);
+constexpr size_t kScratchBytes = kScratchCounterBytes + kScratchAccBytes + kScratchMlBytes;
+static_assert(kScratchCounterBytes % 256 == 0 && kScratchAccBytes % 256 == 0, "256-byte aligned parts");
+}  // namespace
+
+// The array, 4.3 MiB: one copy per device that loads the library, held until
+// the process ends.  Host code never uses this name as an address: its device
+// address comes from hipGetSymbolAddress (scratch_for), once per device.
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
 using apex::fail;
 
 constexpr int kMaxDevices = 64;
@@ -57,10 +77,17 @@ struct DeviceState {
     Buffer counters;   // zeroed at allocation; calls leave it zero
     Buffer partials;
     Buffer error_word;   // input-check error bits, zeroed at allocation and when read
+    char* scratch_addr = nullptr;   // device address of this device's static scratch array
 };
 
 std::mutex g_mutex;
 DeviceState g_dev[kMaxDevices];
+
+
+__global__ void clear_words(int32_t* words, int n)
+{
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) words[i] = 0;
+}
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -111,6 +138,30 @@ int default_workers(int dev, int G, int64_t* out, int* cus = nullptr)
     }
     *out = (int64_t)s.num_cu * s.resident[gi];
     if (cus) *cus = s.num_cu;
+    return APEX_OK;
+}
+
+// Device address of the static scratch on device dev (current), looked up on
+// the device's first no-allocation call; that call also clears the counters
+// with a kernel on `stream` (a kernel, not a memset, so that a call under
+// stream capture records nothing the graph cannot replay).  The array starts
+// zeroed and every launch leaves the counters zero.
+int scratch_for(int dev, hipStream_t stream, char** out)
+{
+    if (dev < 0 || dev >= kMaxDevices) return fail(APEX_ERR_HIP, "device ordinal %d out of range", dev);
+    std::lock_guard<std::mutex> lock(g_mutex);
+    DeviceState& s = g_dev[dev];
+    if (!s.scratch_addr) {
+        void* ptr = nullptr;
+        hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(::scratch));
+        if (e != hipSuccess || !ptr)
+            return fail(APEX_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+        clear_words<<<64, 256, 0, stream>>>((int32_t*)ptr, (int)kScratchPairs);
+        e = hipGetLastError();
+        if (e != hipSuccess) return fail(APEX_ERR_HIP, "clearing the scratch counters: %s", hipGetErrorString(e));
+        s.scratch_addr = (char*)ptr;
+    }
+    *out = s.scratch_addr;
     return APEX_OK;
 }
 
@@ -221,9 +272,9 @@ int dispatch(int G, bool check, bool append, const apex::AttnParams& p, const in
 }
 
 // Validates a call and enqueues its kernel.  The arrival counters and the
-// partials come from the caller's workspace or the library-owned workspace of
-// the device.
-int enqueue(const apex_decode_args& a)
+// partials come from the caller's workspace, the library-owned workspace of
+// the device, or (noalloc) the device's static scratch array.
+int enqueue(const apex_decode_args& a, bool noalloc)
 {
     int rc = check_shapes(a.B, a.Hq, a.Hkv, a.d, a.block_size);
     if (rc != APEX_OK) return rc;
@@ -281,6 +332,11 @@ int enqueue(const apex_decode_args& a)
             return fail(APEX_ERR_INVALID_ARG, "out overlaps k_new or v_new");
     }
 
+    if (noalloc && (int64_t)a.B * a.Hkv > kScratchPairs)
+        return fail(APEX_ERR_UNSUPPORTED,
+                    "B * Hkv = %lld (request, kv-head) pairs exceed the static scratch's %lld",
+                    (long long)a.B * a.Hkv, (long long)kScratchPairs);
+
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return fail(APEX_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
@@ -291,12 +347,22 @@ int enqueue(const apex_decode_args& a)
         rc = default_workers(dev, G, &workers, &cus);
         if (rc != APEX_OK) return rc;
     }
+    // the static scratch holds the partials of kScratchWorkerHeads / G work groups
+    if (noalloc && workers > kScratchWorkerHeads / G) workers = kScratchWorkerHeads / G;
 
     const size_t cbytes = counter_bytes(a.B, a.Hkv);
     const size_t pbytes = partial_bytes(workers, G);
     void* counters = nullptr;
     void* partials = nullptr;
-    if (a.workspace) {
+    void* part_ml = nullptr;
+    if (noalloc) {
+        char* base = nullptr;
+        rc = scratch_for(dev, (hipStream_t)a.stream, &base);
+        if (rc != APEX_OK) return rc;
+        counters = base;
+        partials = base + kScratchCounterBytes;
+        part_ml = base + kScratchCounterBytes + kScratchAccBytes;
+    } else if (a.workspace) {
         if (a.workspace_bytes < cbytes + pbytes)
             return fail(APEX_ERR_OUT_OF_MEMORY, "caller workspace holds %zu bytes, %zu needed",
                         a.workspace_bytes, cbytes + pbytes);
@@ -329,8 +395,9 @@ int enqueue(const apex_decode_args& a)
     p.lse = a.lse_out;
     p.counters = (int32_t*)counters;
     p.pacc = (float*)partials;
-    p.pml = (float*)((char*)partials +
-                     align_up(sizeof(float) * 2 * (size_t)workers * G * apex::kHeadDim, 256));
+    p.pml = part_ml ? (float*)part_ml
+                    : (float*)((char*)partials +
+                               align_up(sizeof(float) * 2 * (size_t)workers * G * apex::kHeadDim, 256));
     p.bt_stride = a.block_table_stride;
     p.scale_log2 = a.scale * 1.4426950408889634f;
     p.B = a.B;
@@ -422,7 +489,7 @@ int apex_decode_attention_ex(const apex_decode_args* args)
 {
     apex::clear_error();
     if (!args) return fail(APEX_ERR_INVALID_ARG, "args is NULL");
-    return enqueue(*args);
+    return enqueue(*args, false);
 }
 
 int apex_decode_attention(const void* q, const void* k_cache, const void* v_cache,
@@ -445,6 +512,30 @@ int apex_decode_attention(const void* q, const void* k_cache, const void* v_cach
     a.scale = scale;
     a.stream = stream;
     return apex_decode_attention_ex(&a);
+}
+
+int apex_decode_attention_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                                  const int32_t* block_table, const int32_t* context_lens, void* out,
+                                  int B, int Hq, int Hkv, int d, int block_size, float scale,
+                                  void* stream)
+{
+    apex::clear_error();
+    apex_decode_args a;
+    memset(&a, 0, sizeof(a));
+    a.q = q;
+    a.k_cache = k_cache;
+    a.v_cache = v_cache;
+    a.block_table = block_table;
+    a.context_lens = context_lens;
+    a.out = out;
+    a.B = B;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.d = d;
+    a.block_size = block_size;
+    a.scale = scale;
+    a.stream = stream;
+    return enqueue(a, true);
 }
 
 int apex_decode_check_device_error(uint32_t* error_bits)

@@ -437,3 +437,26 @@ def test_partition_huge_unit_counts_divide_exactly(lib):
                 assert p["contributors"][b, g] == want, (launched, b, g)
             pre += nb
 
+
+# ---------------------------------------------------------------------------
+# apex_decode_attention_noalloc: the same validation, plus the static
+# scratch's pair limit (host checks, before any HIP call)
+# ---------------------------------------------------------------------------
+
+def noalloc_call(lib, B=2, Hq=32, Hkv=8, q=FAKE, out=FAKE + (5 << 30)):
+    return lib.apex_decode_attention_noalloc(q, FAKE + (1 << 30), FAKE + (2 << 30), FAKE + (3 << 30),
+                                             FAKE + (4 << 30), out, B, Hq, Hkv, 128, 16, 0.1, None)
+
+
+def test_noalloc_refuses_more_pairs_than_its_scratch(lib):
+    assert noalloc_call(lib, B=8193, Hq=8, Hkv=8) == A.APEX_ERR_UNSUPPORTED
+    assert "65536" in A.last_error()
+    assert noalloc_call(lib, B=2049, Hq=32, Hkv=32) == A.APEX_ERR_UNSUPPORTED
+
+
+def test_noalloc_validates_like_the_base_call(lib):
+    assert noalloc_call(lib, Hq=30) == A.APEX_ERR_INVALID_ARG
+    assert noalloc_call(lib, q=0) == A.APEX_ERR_INVALID_ARG
+    assert noalloc_call(lib, out=FAKE + 64) == A.APEX_ERR_INVALID_ARG
+    assert noalloc_call(lib, B=0, q=0, out=0) == A.APEX_OK
+    assert A.last_error() == ""
