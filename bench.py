@@ -89,11 +89,14 @@ def log(msg):
 
 
 def _code_only(text):
-    """C++ source without comments and with whitespace runs collapsed, so that
-    editing a comment does not invalidate a counter summary."""
+    """C++ source of the product build: comments and the blocks of the
+    work-group trace build (APEX_TRACE_WORK_GROUPS, never defined in the
+    product) removed and whitespace runs collapsed, so that editing a comment
+    or the diagnostic build does not invalidate a counter summary."""
     import re
     text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
     text = re.sub(r"//[^\n]*", " ", text)
+    text = re.sub(r"#ifdef APEX_TRACE_WORK_GROUPS\b.*?#endif", " ", text, flags=re.S)
     return " ".join(text.split())
 
 

@@ -13,10 +13,12 @@ CPU_LIB = os.path.join(HERE, "libapex_cpu.so")
 CPU_DIR = os.path.join(CSRC, "cpu")
 OVERLAP_LIB = os.path.join(HERE, "libapex_overlap.so")
 OVERLAP_SOURCES = [os.path.join(CSRC, "overlap", "overlap.hip")]
+TRACE_LIB = os.path.join(HERE, "libapex_decode_trace.so")
 PROBE_LIB = os.path.join(HERE, "libapex_hbm_probe.so")
 PROBE_SOURCES = [os.path.join(CSRC, "hbm_probe.hip")]
 HEADERS = [os.path.join(ROOT, "include", "apex_decode.h"),
            os.path.join(ROOT, "include", "apex_kv_append.h"),
+           os.path.join(ROOT, "include", "apex_decode_trace.h"),
            os.path.join(CSRC, "kernels.h"), os.path.join(CSRC, "plan_policy.h"),
            os.path.join(CSRC, "status.h")]
 
@@ -71,11 +73,13 @@ def build_cpu(out=CPU_LIB, quiet=False):
 
 
 def build(out=LIB, extra=(), quiet=False):
-    """Compile the decode-attention library, the host attention backend, the
-    overlap runtime (linked against the host backend) and the HBM probe
+    """Compile the decode-attention library, its work-group trace build (the
+    same sources with APEX_TRACE_WORK_GROUPS), the host attention backend,
+    the overlap runtime (linked against the host backend) and the HBM probe
     library."""
     build_cpu(quiet=quiet)
     _compile(PROBE_SOURCES, PROBE_LIB, extra, quiet)
+    _compile(SOURCES, TRACE_LIB, [*extra, "-DAPEX_TRACE_WORK_GROUPS"], quiet)
     _compile(OVERLAP_SOURCES, OVERLAP_LIB,
              [*extra, "-L", HERE, "-lapex_cpu", "-Wl,-rpath,$ORIGIN", "-pthread"], quiet)
     return _compile(SOURCES, out, extra, quiet)

@@ -13,6 +13,9 @@
 #include <string.h>
 
 #include "apex_decode.h"
+#ifdef APEX_TRACE_WORK_GROUPS
+#include "apex_decode_trace.h"
+#endif
 #include "kernels.h"
 #include "plan_policy.h"
 #include "status.h"
@@ -82,6 +85,12 @@ struct DeviceState {
 
 std::mutex g_mutex;
 DeviceState g_dev[kMaxDevices];
+
+#ifdef APEX_TRACE_WORK_GROUPS
+// work-group timeline buffer of the diagnostic build (apex_decode_trace.h)
+uint64_t* g_trace = nullptr;
+int64_t g_trace_groups = 0;
+#endif
 
 
 __global__ void clear_words(int32_t* words, int n)
@@ -412,6 +421,13 @@ int enqueue(const apex_decode_args& a, bool noalloc)
     p.new_stride = new_stride;
     p.k_store = (apex::f16*)a.k_cache;
     p.v_store = (apex::f16*)a.v_cache;
+#ifdef APEX_TRACE_WORK_GROUPS
+    {
+        std::lock_guard<std::mutex> lock(g_mutex);
+        p.trace = g_trace;
+        p.trace_groups = g_trace_groups;
+    }
+#endif
 
     hipStream_t stream = (hipStream_t)a.stream;
     const int32_t* bt = a.block_table;
@@ -537,6 +553,20 @@ int apex_decode_attention_noalloc(const void* q, const void* k_cache, const void
     a.stream = stream;
     return enqueue(a, true);
 }
+
+#ifdef APEX_TRACE_WORK_GROUPS
+int apex_decode_trace_buffer(void* device_words, int64_t max_work_groups)
+{
+    apex::clear_error();
+    if (max_work_groups < 0) return fail(APEX_ERR_INVALID_ARG, "max_work_groups is negative");
+    if (device_words && !aligned(device_words, 8))
+        return fail(APEX_ERR_INVALID_ARG, "the trace buffer must be 8-byte aligned");
+    std::lock_guard<std::mutex> lock(g_mutex);
+    g_trace = device_words ? (uint64_t*)device_words : nullptr;
+    g_trace_groups = device_words ? max_work_groups : 0;
+    return APEX_OK;
+}
+#endif
 
 int apex_decode_check_device_error(uint32_t* error_bits)
 {

@@ -77,7 +77,23 @@ struct AttnParams {
     int64_t new_stride;
     f16* k_store;          // the caches, written by the fused append
     f16* v_store;
+#ifdef APEX_TRACE_WORK_GROUPS
+    uint64_t* trace;       // [trace_groups][kTraceWords] work-group timeline, or null
+    int64_t trace_groups;
+#endif
 };
+
+#ifdef APEX_TRACE_WORK_GROUPS
+// Work-group timeline of the diagnostic build: per work group, in ticks of
+// the 100 MHz real-time clock, its first instruction, the end of its
+// partition prologue, the completion of wave 0's first tiles and its end;
+// then its segments, the split ones among them, and its units.
+constexpr int kTraceWords = 8;
+__device__ inline uint64_t trace_clock() { return __builtin_amdgcn_s_memrealtime(); }
+// the work group's row, kept in LDS while it runs (no register stays live
+// across the block loop for it)
+__shared__ uint64_t s_trace[kTraceWords];
+#endif
 
 // Input-check error bits (apex_decode.h: APEX_DEVICE_ERR_*).
 constexpr unsigned kErrBlockId = 1u;      // a block id outside [0, num_blocks)
@@ -397,6 +413,9 @@ __device__ inline void wave_attend(const AttnParams& p, const WaveSeg& cs, const
     // segment ahead) is complete from here on, so the loop's own waits are
     // those of its two-deep pipeline alone.
     __builtin_amdgcn_s_waitcnt(0);
+#ifdef APEX_TRACE_WORK_GROUPS
+    if (wave == 0 && lane == 0 && s_trace[2] == 0) s_trace[2] = trace_clock();
+#endif
     if (kAppend && uniform(wave) == 0) new_token_logits<G>(p, nt, lane, s_new);
 #pragma unroll
     for (int i = 0; i < 4; ++i) st.qop[i] = st.qnext[i];
@@ -599,6 +618,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     const int64_t w = blockIdx.x;
     const int B = p.B;
     const bool cached = B <= kCachedLens;
+#ifdef APEX_TRACE_WORK_GROUPS
+    if (tid < kTraceWords) s_trace[tid] = tid == 0 ? trace_clock() : 0;
+#endif
 
     // 1. partition.  context_lens is read from memory once: each thread sums
     // the blocks of a contiguous run of requests (and keeps the lengths in
@@ -713,6 +735,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
 
     // 2. segments.  Each one is announced to the waves together with the
     // next, so their K/V pipelines run on from one to the other.
+#ifdef APEX_TRACE_WORK_GROUPS
+    if (tid == 0) s_trace[1] = trace_clock();
+#endif
     int take = (int)min((int64_t)(nb - blk), u1 - u);
     WaveSeg cs = wave_seg<G>(p, bt + (size_t)uniform(b) * (size_t)stride, b, g, blk, blk + take, wave, lane);
     WaveTiles st;
@@ -733,6 +758,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
                                         more && take >= kPrefetchBlocks && take2 >= kPrefetchBlocks, L,
                                         st, wave, lane, s_acc, s_m, s_l, s_new);
         __syncthreads();
+#ifdef APEX_TRACE_WORK_GROUPS
+        if (tid == 0) ++s_trace[4];
+#endif
 
         // 3. merge the waves, emit rows or a partial
         const int64_t p0 = pre * p.Hkv + (int64_t)g * nb;
@@ -768,6 +796,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
             }
         }
         if (wf != wl) {
+#ifdef APEX_TRACE_WORK_GROUPS
+            if (tid == 0) ++s_trace[5];
+#endif
             // The partials are written with device-coherent stores; waiting for
             // them to complete before the arrival is counted makes them visible
             // to the last arriver's device-coherent loads, on whichever XCD it
@@ -873,6 +904,19 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
             for (int i = tid; i < p.Hq * D; i += kAttnThreads) write_row(p, b, i / D, i % D, 0.f, 0.f, 0.f);
         }
     }
+#ifdef APEX_TRACE_WORK_GROUPS
+    if (p.trace && tid == 0 && w < p.trace_groups) {
+        uint64_t* t = p.trace + w * kTraceWords;
+        t[0] = s_trace[0];
+        t[1] = s_trace[1];
+        t[2] = s_trace[2];
+        t[3] = trace_clock();
+        t[4] = s_trace[4];
+        t[5] = s_trace[5];
+        t[6] = (uint64_t)(u1 - u0);
+        t[7] = 0;
+    }
+#endif
 }
 
 }  // namespace apex

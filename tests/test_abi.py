@@ -460,3 +460,44 @@ def test_noalloc_validates_like_the_base_call(lib):
     assert noalloc_call(lib, out=FAKE + 64) == A.APEX_ERR_INVALID_ARG
     assert noalloc_call(lib, B=0, q=0, out=0) == A.APEX_OK
     assert A.last_error() == ""
+
+
+# ---------------------------------------------------------------------------
+# the work-group trace build (libapex_decode_trace.so): the product library's
+# symbols plus apex_decode_trace_buffer, which the product does not export
+# ---------------------------------------------------------------------------
+
+@pytest.fixture(scope="module")
+def trace_lib(lib):
+    from paper_2506_03296_amd import wg_trace
+    return wg_trace.load_trace_library()
+
+
+def test_trace_build_exports_the_trace_entry_point_and_the_product_does_not(lib, trace_lib):
+    for name in declared_functions():
+        assert hasattr(trace_lib, name), name
+    assert hasattr(trace_lib, "apex_decode_trace_buffer")
+    with pytest.raises(AttributeError):
+        lib.apex_decode_trace_buffer
+
+
+def test_trace_buffer_arguments(trace_lib):
+    assert trace_lib.apex_decode_trace_buffer(FAKE + 4, 16) == A.APEX_ERR_INVALID_ARG
+    assert trace_lib.apex_decode_trace_buffer(FAKE, -1) == A.APEX_ERR_INVALID_ARG
+    assert trace_lib.apex_decode_trace_buffer(FAKE, 16) == A.APEX_OK
+    assert trace_lib.apex_decode_trace_buffer(None, 0) == A.APEX_OK
+
+
+def test_trace_summary_of_a_synthetic_timeline():
+    from paper_2506_03296_amd import wg_trace
+    rows = np.zeros((8, 8), dtype=np.int64)
+    for w in range(8):
+        s = 1000 + 10 * (w % 4) + 100 * (w >= 4)      # second round starts 1 us later
+        rows[w] = [s, s + 200, s + 500, s + 10000 + 100 * w, 1 + w % 2, w % 2, 40, 0]
+    r = wg_trace.summarize(rows, cus=4)
+    assert r["work_groups"] == 8 and r["active"] == 8
+    assert abs(r["prologue"]["p50"] - 2.0) < 1e-9 and abs(r["first_load"]["p50"] - 3.0) < 1e-9
+    assert abs(r["span"] - (1130 + 10000 + 700 - 1000) * 0.01) < 1e-9     # group 7 ends last
+    assert abs(r["dispatch"]["round2_start_min"] - 1.0) < 1e-9
+    assert r["split_segments"] == 4
+    assert set(r["by_segments"]) == {1, 2}
