@@ -50,10 +50,11 @@
  * unless apex_decode_attention_ex is asked to (APEX_DECODE_FLAG_CHECK_INPUTS).
  *
  * Work partition: one persistent kernel launch per call.  Each work group
- * derives the partition from context_lens itself, takes an equal share of
- * the (request, kv-head, block) units, and (request, kv-head) pairs shared by
- * several work groups are merged by a log-sum-exp combine done by the last
- * work group to finish its share of the pair.
+ * derives the partition from context_lens itself, takes an equal-cost share
+ * of the (request, kv-head, block) units (a pair's cost is its blocks plus a
+ * fixed start-up cost), and (request, kv-head) pairs shared by several work
+ * groups are merged by a log-sum-exp combine done by the last work group to
+ * finish its share of the pair.
  */
 #ifndef APEX_DECODE_H
 #define APEX_DECODE_H
@@ -107,12 +108,14 @@ typedef struct apex_decode_args {
     int64_t block_table_stride;
     /* work groups of the persistent launch; 0 = as many as the device keeps
      * resident.  The work (one unit = one 16-token block of one kv-head) is
-     * cut into equal contiguous ranges, one per work group; with 0 a range is
-     * never shorter than 16 units unless that would leave fewer ranges than
-     * non-empty (request, kv-head) pairs, and a batch of at most one pair per
-     * CU (and at most 1024 units per CU) uses one work group per CU; with
-     * n > 0 every range holds at least one unit (tests use this to force
-     * split requests) */
+     * cut into contiguous ranges, one per work group.  With 0 the ranges are
+     * of equal cost, where every non-empty (request, kv-head) pair costs its
+     * units plus 8 (the latency of starting and finishing a pair, so that a
+     * run of short pairs is spread over several work groups); about 16 units
+     * per work group, but never fewer work groups than non-empty pairs, and a
+     * batch of at most one pair per CU (and at most 1024 units per CU) uses
+     * one work group per CU.  With n > 0 the ranges hold equal numbers of
+     * units, at least one each (tests use this to force split requests) */
     int num_workers;
     /* caller-owned device workspace of at least apex_decode_workspace_bytes()
      * bytes and 256-byte aligned, or NULL for the library-owned one.  Its
@@ -201,9 +204,10 @@ size_t apex_decode_counter_bytes(int B, int Hkv);
  * Host mirror of the work partition, for inspection and tests (no GPU
  * needed).  Inputs: host context_lens[B], Hkv, block_size, the number of
  * launched work groups, whether that number was forced (num_workers > 0 in
- * apex_decode_args), and the device's compute units (the default grid uses
- * only one work group per CU for a batch of at most one (request, kv-head)
- * pair per CU and at most 1024 units per CU; 0 leaves that rule out).
+ * apex_decode_args: forced grids cut equal units, the default grid equal
+ * costs), and the device's compute units (the default grid uses only one
+ * work group per CU for a batch of at most one (request, kv-head) pair per
+ * CU and at most 1024 units per CU; 0 leaves that rule out).
  * Outputs (any may be NULL): contributors_out[B * Hkv] = work groups that
  * share each (request, kv-head) pair (1 = written directly, more = combined
  * from partials), *units_out = blocks x kv-heads, *active_out = work groups

@@ -413,6 +413,7 @@ int enqueue(const apex_decode_args& a, bool noalloc)
     p.Hq = a.Hq;
     p.Hkv = a.Hkv;
     p.min_units = a.num_workers > 0 ? 1 : apex::kMinUnitsPerWorker;
+    p.seg_cost = a.num_workers > 0 ? 0 : apex::kSegmentCostUnits;
     p.cus = cus;
     p.num_blocks = check ? a.num_blocks : 0;
     p.error_word = (unsigned*)error_word;
@@ -478,22 +479,26 @@ int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block
         nonempty += context_lens[b] > 0;
     }
     const int64_t units = blocks * Hkv;
+    const int64_t pairs = nonempty * Hkv;
     const int64_t W = apex::active_workers(units, launched_workers,
-                                           forced ? 1 : apex::kMinUnitsPerWorker, nonempty * Hkv,
+                                           forced ? 1 : apex::kMinUnitsPerWorker, pairs,
                                            forced ? 0 : cus);
-    int64_t partials = 0, pre = 0;
+    const int64_t K = forced ? 0 : apex::kSegmentCostUnits;
+    const int64_t V = units + K * pairs;
+    int64_t partials = 0, pre = 0, pp = 0;
     for (int b = 0; b < B; ++b) {
         const int64_t nb = apex::blocks_of(context_lens[b], block_size);
         for (int g = 0; g < Hkv; ++g) {
             int64_t n = 0;
             if (nb > 0) {
-                const int64_t p0 = pre * Hkv + (int64_t)g * nb;
-                n = apex::worker_of(p0 + nb - 1, units, W) - apex::worker_of(p0, units, W) + 1;
+                const int64_t vf = apex::first_block_position(pre * Hkv + (int64_t)g * nb, pp * Hkv + g, K);
+                n = apex::worker_of(vf + nb - 1, V, W) - apex::worker_of(vf, V, W) + 1;
                 if (n > 1) partials += n;
             }
             if (contributors_out) contributors_out[(size_t)b * Hkv + g] = (int32_t)n;
         }
         pre += nb;
+        pp += nb > 0;
     }
     if (units_out) *units_out = units;
     if (active_out) *active_out = units > 0 ? W : 0;

@@ -64,6 +64,7 @@ struct AttnParams {
     int Hq;
     int Hkv;
     int min_units;         // minimum units per active worker
+    int seg_cost;          // cost positions charged per pair (plan_policy.h), 0 = equal units
     int cus;               // compute units for the one-group-per-CU rule (0 = off)
     int64_t num_blocks;    // physical blocks in the caches (input check only)
     unsigned* error_word;  // input-check error bits (input check only)
@@ -609,6 +610,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     __shared__ int s_wcnt[kWaves];
     __shared__ int s_loc_b;
     __shared__ int64_t s_loc_pre;
+    __shared__ int s_loc_g;
+    __shared__ int s_loc_blk;
+    __shared__ int64_t s_loc_vf;
     __shared__ int s_last;
     __shared__ float s_new[G];
 
@@ -655,19 +659,23 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         tmax = max(tmax, (int)blocks_of(is_cut(raw) ? (int)row_tokens : raw, kBlockSize));
         tcnt += nb > 0;
     }
+    const int own_cnt = tcnt;
     int incl = wave_incl_sum(tsum);
     tmax = wave_incl_max(tmax);
-    tcnt = wave_incl_sum(tcnt);
+    int incl_cnt = wave_incl_sum(tcnt);
     if (lane == 63) {
         s_wsum[wave] = incl;
         s_wmax[wave] = tmax;
-        s_wcnt[wave] = tcnt;
+        s_wcnt[wave] = incl_cnt;
     }
     __syncthreads();
     int total = 0, maxb = 0, nonempty = 0;
 #pragma unroll
     for (int v = 0; v < kWaves; ++v) {
-        if (v < wave) incl += s_wsum[v];
+        if (v < wave) {
+            incl += s_wsum[v];
+            incl_cnt += s_wcnt[v];
+        }
         total += s_wsum[v];
         maxb = max(maxb, s_wmax[v]);
         nonempty += s_wcnt[v];
@@ -675,60 +683,89 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     auto len_of = [&](int b) -> int { return cached ? s_lens[b] : cached_len(lens[b]); };
 
     const int64_t units = (int64_t)uniform(total) * p.Hkv;
+    const int64_t pairs = (int64_t)uniform(nonempty) * p.Hkv;
     const int64_t stride = p.bt_stride > 0 ? p.bt_stride : (int64_t)uniform(maxb);
-    const int64_t W = active_workers(units, (int64_t)gridDim.x, p.min_units,
-                                     (int64_t)uniform(nonempty) * p.Hkv, p.cus);
-    const int64_t u0 = units > 0 && w < W ? worker_start(w, units, W) : 0;
-    const int64_t u1 = units > 0 && w < W ? worker_start(w + 1, units, W) : 0;
+    const int64_t W = active_workers(units, (int64_t)gridDim.x, p.min_units, pairs, p.cus);
+    // the cost line: every non-empty pair's K cost positions, then its blocks
+    const int64_t K = p.seg_cost;
+    const int64_t V = units + K * pairs;
+    const int64_t v0 = units > 0 && w < W ? worker_start(w, V, W) : 0;
+    const int64_t v1 = units > 0 && w < W ? worker_start(w + 1, V, W) : 0;
 
-    if (u0 < u1) {
-    // locate the pair holding unit u0
-    {
-        const int64_t excl = incl - tsum;
-        if (excl * p.Hkv <= u0 && u0 < (int64_t)incl * p.Hkv) {
-            int64_t pre = excl;
+    // The worker's blocks are those whose positions lie in [v0, v1).  Request
+    // b's positions start at Hkv (pre_b + K pp_b) (pre_b blocks and pp_b
+    // non-empty requests before it) and number Hkv (nb_b + K); the thread
+    // whose requests hold v0 finds the pair there and its first block at or
+    // after v0 (block 0 when v0 is one of the pair's cost positions), and
+    // publishes the pair, that block and the position of the pair's block 0.
+    if (v0 < v1) {
+        const int64_t hk = p.Hkv;
+        const int64_t lo = (int64_t)(incl - tsum) + K * (incl_cnt - own_cnt);
+        const int64_t hi = (int64_t)incl + K * incl_cnt;
+        if (lo * hk <= v0 && v0 < hi * hk) {
+            int64_t pre = incl - tsum, vpre = lo * hk;
             for (int b = r0; b < r1; ++b) {
-                const int64_t nb = blocks_of(len_of(b), kBlockSize);
-                if (u0 < (pre + nb) * p.Hkv) {
+                const int nb = (int)blocks_of(len_of(b), kBlockSize);
+                if (nb == 0) continue;
+                const int64_t span = (int64_t)(nb + K) * hk;
+                if (v0 < vpre + span) {
+                    const int64_t g = div_floor(v0 - vpre, nb + K);
+                    const int64_t vf = vpre + g * (nb + K) + K;   // position of the pair's block 0
                     s_loc_b = b;
                     s_loc_pre = pre;
+                    s_loc_g = (int)g;
+                    s_loc_blk = (int)(v0 > vf ? v0 - vf : 0);
+                    s_loc_vf = vf;
                     break;
                 }
                 pre += nb;
+                vpre += span;
             }
         }
     }
     __syncthreads();
 
-    int b = uniform(s_loc_b);
-    int64_t pre = uniform64(s_loc_pre);
-    int L = uniform(len_of(b));
-    int nb = (int)blocks_of(L, kBlockSize);
-    int64_t off = u0 - pre * p.Hkv;
-    const int64_t gq = div_floor(off, nb);
-    int g = uniform((int)gq);
-    int blk = uniform((int)(off - gq * nb));
-    int64_t u = u0;
+    // A segment is the worker's blocks of one pair: from block blk of the pair
+    // whose block 0 lies at position vf, up to the pair's end or the worker's
+    // range end v1, whichever comes first (none when v1 falls on or before
+    // the block: the range ends among cost positions).
+    auto seg_take = [&](int nb_, int blk_, int64_t vf_) -> int {
+        const int64_t left = v1 - (vf_ + blk_);
+        return left <= 0 ? 0 : (int)min((int64_t)(nb_ - blk_), left);
+    };
+    int b = 0, g = 0, blk = 0, L = 0, nb = 0, take = 0;
+    int64_t pre = 0, vf = 0;
+    if (v0 < v1) {
+        b = uniform(s_loc_b);
+        pre = uniform64(s_loc_pre);
+        g = uniform(s_loc_g);
+        blk = uniform(s_loc_blk);
+        vf = uniform64(s_loc_vf);
+        L = uniform(len_of(b));
+        nb = (int)blocks_of(L, kBlockSize);
+        take = seg_take(nb, blk, vf);
+    }
 
-    // Moves a segment cursor past the `take` units of its segment; false when
-    // the worker's range is done.
-    auto advance = [&](int& b_, int64_t& pre_, int& L_, int& nb_, int& g_, int& blk_, int64_t& u_,
+    if (take > 0) {
+    // Moves a segment cursor past its segment to the worker's next one;
+    // false when the worker's range is done.
+    auto advance = [&](int& b_, int64_t& pre_, int& L_, int& nb_, int& g_, int& blk_, int64_t& vf_,
                        int take_) -> bool {
-        u_ += take_;
-        if (u_ >= u1) return false;
         blk_ += take_;
-        if (blk_ == nb_) {
-            blk_ = 0;
-            if (++g_ == p.Hkv) {
-                g_ = 0;
-                pre_ += nb_;
-                do {
-                    ++b_;
-                } while (b_ < B && len_of(b_) <= 0);
-                if (b_ >= B) return false;   // unreachable: units remain after the current pair
-                L_ = uniform(len_of(b_));
-                nb_ = (int)blocks_of(L_, kBlockSize);
-            }
+        if (blk_ < nb_) return false;   // the range ended inside the pair
+        const int64_t vnext = vf_ + nb_ + K;   // the next pair's block 0
+        if (v1 <= vnext) return false;
+        blk_ = 0;
+        vf_ = vnext;
+        if (++g_ == p.Hkv) {
+            g_ = 0;
+            pre_ += nb_;
+            do {
+                ++b_;
+            } while (b_ < B && len_of(b_) <= 0);
+            if (b_ >= B) return false;   // unreachable: positions remain after the current pair
+            L_ = uniform(len_of(b_));
+            nb_ = (int)blocks_of(L_, kBlockSize);
         }
         return true;
     };
@@ -738,7 +775,6 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
 #ifdef APEX_TRACE_WORK_GROUPS
     if (tid == 0) s_trace[1] = trace_clock();
 #endif
-    int take = (int)min((int64_t)(nb - blk), u1 - u);
     WaveSeg cs = wave_seg<G>(p, bt + (size_t)uniform(b) * (size_t)stride, b, g, blk, blk + take, wave, lane);
     WaveTiles st;
     st.prefetched = false;
@@ -746,9 +782,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     load_q<G>(st.qnext, cs, lane);
     while (true) {
         int b2 = b, L2 = L, nb2 = nb, g2 = g, blk2 = blk;
-        int64_t pre2 = pre, u2 = u;
-        const bool more = advance(b2, pre2, L2, nb2, g2, blk2, u2, take);
-        const int take2 = more ? (int)min((int64_t)(nb2 - blk2), u1 - u2) : 0;
+        int64_t pre2 = pre, vf2 = vf;
+        const bool more = advance(b2, pre2, L2, nb2, g2, blk2, vf2, take);
+        const int take2 = more ? seg_take(nb2, blk2, vf2) : 0;
         WaveSeg ns = cs;
         ns.n = 0;
         if (more)
@@ -759,14 +795,16 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
                                         st, wave, lane, s_acc, s_m, s_l, s_new);
         __syncthreads();
 #ifdef APEX_TRACE_WORK_GROUPS
-        if (tid == 0) ++s_trace[4];
+        if (tid == 0) {
+            ++s_trace[4];
+            s_trace[6] += take;
+        }
 #endif
 
         // 3. merge the waves, emit rows or a partial
-        const int64_t p0 = pre * p.Hkv + (int64_t)g * nb;
-        const int64_t wf = worker_of(p0, units, W);
-        const int64_t wl = worker_of(p0 + nb - 1, units, W);
-        const int64_t slot = u0 < p0 ? 2 * w + 1 : 2 * w;   // partial_slot(w, p0, units, W)
+        const int64_t wf = worker_of(vf, V, W);
+        const int64_t wl = worker_of(vf + nb - 1, V, W);
+        const int64_t slot = partial_slot(w, wf);
         for (int idx = tid; idx < G * D; idx += kAttnThreads) {
             const int h = idx / D, dim = idx % D;
             float M = s_m[0][h];
@@ -818,9 +856,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
                 // kCombineChunk contributors at once, then folds them in with
                 // an online rescale (running max M, numerator, denominator)
                 const int nc = (int)(wl - wf + 1);
-                // every contributor after the first starts inside the pair,
-                // so its slot is 2v (its first segment)
-                const int64_t first_slot = partial_slot(wf, p0, units, W);
+                // the first contributor's slot is 2wf + 1; every later one
+                // starts inside the pair, so its slot is 2v (partial_slot)
+                const int64_t first_slot = partial_slot(wf, wf);
                 for (int idx = tid; idx < G * D; idx += kAttnThreads) {
                     const int h = idx / D, dim = idx % D;
                     float M = -INFINITY, num = 0.f, den = 0.f;
@@ -867,11 +905,11 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         if (!more) break;
         b = b2;
         pre = pre2;
+        vf = vf2;
         L = L2;
         nb = nb2;
         g = g2;
         blk = blk2;
-        u = u2;
         take = take2;
         cs = ns;
     }
@@ -913,7 +951,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         t[3] = trace_clock();
         t[4] = s_trace[4];
         t[5] = s_trace[5];
-        t[6] = (uint64_t)(u1 - u0);
+        t[6] = s_trace[6];
         t[7] = 0;
     }
 #endif

@@ -5,12 +5,19 @@
 // step).  A batch is ragged -- a few long requests next to many short ones --
 // so the work is cut by amount, not by request.  One unit is one block of one
 // kv-head (16 tokens: 4 KiB of K plus 4 KiB of V at d = 128); the units are
-// laid out in (request b, kv-head g, block) order and worker w of W takes the
-// contiguous range [floor(w U / W), floor((w + 1) U / W)).  Every worker does
-// the same number of units whatever the length mix; a (request, kv-head) pair
-// whose units straddle workers is finished by a log-sum-exp combine of the
-// workers' partial results.  Each worker has at most two partial segments
-// (its first and its last), which fixes where they are stored.
+// laid out in (request b, kv-head g, block) order.  Besides its units, a
+// worker pays a fixed cost for every (request, kv-head) pair it attends --
+// the block-id and first-tile latency, the merge and the emit -- so each
+// non-empty pair is charged K = kSegmentCostUnits extra positions: on a line
+// of V = U + K P positions (P pairs) every pair has its K cost positions
+// followed by its blocks, and worker w of W takes the positions
+// [floor(w V / W), floor((w + 1) V / W)).  The blocks among them form a
+// contiguous range of units, so every worker walks consecutive units as
+// before, and a run of short pairs no longer lands on one worker.  A
+// (request, kv-head) pair whose units straddle workers is finished by a
+// log-sum-exp combine of the workers' partial results.  Each worker has at
+// most two partial segments (its first and its last), which fixes where
+// they are stored.  Forced grids (tests) take K = 0: equal units.
 //
 // These functions are compiled for both the host (inspection, tests) and the
 // device (every worker runs them on its own), so both see the same partition.
@@ -25,6 +32,10 @@ constexpr int kHeadDim = 128;
 constexpr int kBlockSize = 16;
 constexpr int kMinUnitsPerWorker = 16;  // four blocks per wave of a 4-wave work group
 constexpr int64_t kUnitsPerCuForOne = 1024;   // 8 MiB of K/V per CU
+// Cost of a pair's segment in units: a short segment takes about 2-3 us of
+// latency (block ids, first tiles, merge, emit), the time a work group
+// streams about eight blocks in.
+constexpr int kSegmentCostUnits = 8;
 
 // floor(a / b) for a >= 0, b > 0.  A 64-bit division is a long software
 // sequence on the GPU; the partition's operands nearly always fit in 32 bits,
@@ -59,24 +70,34 @@ __host__ __device__ inline int64_t active_workers(int64_t units, int64_t launche
     return w < launched ? w : launched;
 }
 
-// First unit of worker w (the range of w is [worker_start(w), worker_start(w+1))).
-__host__ __device__ inline int64_t worker_start(int64_t w, int64_t units, int64_t workers)
+// First position of worker w on the cost line of `positions` positions (the
+// range of w is [worker_start(w), worker_start(w+1))).
+__host__ __device__ inline int64_t worker_start(int64_t w, int64_t positions, int64_t workers)
 {
-    return div_floor(w * units, workers);
+    return div_floor(w * positions, workers);
 }
 
-// The worker whose range holds unit u (0 <= u < units).
-__host__ __device__ inline int64_t worker_of(int64_t u, int64_t units, int64_t workers)
+// The worker whose range holds position v (0 <= v < positions).
+__host__ __device__ inline int64_t worker_of(int64_t v, int64_t positions, int64_t workers)
 {
-    return div_floor((u + 1) * workers - 1, units);
+    return div_floor((v + 1) * workers - 1, positions);
 }
 
-// Partial slot that worker w uses for the pair whose units start at p0:
-// 2w for the worker's first segment, 2w + 1 for its last one.
-__host__ __device__ inline int64_t partial_slot(int64_t w, int64_t p0, int64_t units,
-                                                int64_t workers)
+// Position of the first block of the pair with index `pair` (in (request,
+// kv-head) order over the non-empty pairs) whose units start at unit p0:
+// every pair up to and including it adds its K cost positions.
+__host__ __device__ inline int64_t first_block_position(int64_t p0, int64_t pair, int64_t K)
 {
-    return worker_start(w, units, workers) < p0 ? 2 * w + 1 : 2 * w;
+    return p0 + K * (pair + 1);
+}
+
+// Partial slot that worker w uses for a split pair whose first contributor
+// is wf: the first contributor holds the pair's start and runs past its
+// range, so the pair is its last segment (slot 2w + 1); every later one
+// starts inside the pair, so the pair is its first segment (slot 2w).
+__host__ __device__ inline int64_t partial_slot(int64_t w, int64_t wf)
+{
+    return w == wf ? 2 * w + 1 : 2 * w;
 }
 
 }  // namespace apex

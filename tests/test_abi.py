@@ -70,17 +70,30 @@ def test_args_struct_matches_header_field_order():
 # work partition (host mirror) against a brute-force assignment of units
 # ---------------------------------------------------------------------------
 
+SEG_COST = 8   # cost positions per pair of the default grid (plan_policy.h)
+
+
 def _brute_partition(lens, Hkv, launched, forced, cus=0):
+    """Owner of every unit, from an explicit line of positions: each non-empty
+    (request, kv-head) pair's SEG_COST cost positions, then its blocks; worker
+    w takes positions [w V / W, (w + 1) V / W).  Forced grids: no cost."""
     blocks = [(-(-int(L) // 16)) if L > 0 else 0 for L in lens]
     U = sum(blocks) * Hkv
     pairs = sum(1 for nb in blocks if nb > 0) * Hkv
     if not forced and cus > 0 and pairs <= cus and U <= 1024 * cus:
         launched = min(launched, cus)
     W = min(launched, max(1, U // (1 if forced else 16), pairs))
+    K = 0 if forced else SEG_COST
+    line = []                      # True = a block, False = a cost position
+    for nb in blocks:
+        for _ in range(Hkv if nb else 0):
+            line += [False] * K + [True] * nb
+    V = len(line)
+    assert V == U + K * pairs
+    starts = [w * V // W for w in range(W + 1)]
     owner = []
-    starts = [w * U // W for w in range(W + 1)]
     for w in range(W):
-        owner += [w] * (starts[w + 1] - starts[w])
+        owner += [w] * sum(line[starts[w]:starts[w + 1]])
     assert len(owner) == U
     contrib = np.zeros((len(lens), Hkv), dtype=np.int64)
     per_worker_partials = np.zeros(W, dtype=np.int64)
