@@ -485,9 +485,14 @@ __device__ inline void wave_attend(const AttnParams& p, const WaveSeg& cs, const
         f32x4 pw;
 #pragma unroll
         for (int i = 0; i < 4; ++i) pw[i] = exp2_fast(sv[i] - mnew);
+        // the weights as two fp16 MFMA operands: ph = pw rounded to fp16 and
+        // pl = the rest rounded to fp16, together 22 significant bits (the
+        // rest pw - ph is exact in fp32); the normaliser sums the same parts
         const f16x4 ph = __builtin_convertvector(pw, f16x4);
-        // the normaliser uses the same fp16-rounded weights as the numerator
-        l = l * alpha + (((float)ph[0] + (float)ph[1]) + ((float)ph[2] + (float)ph[3]));
+        const f32x4 ph32 = __builtin_convertvector(ph, f32x4);
+        const f16x4 pl = __builtin_convertvector(pw - ph32, f16x4);
+        const f32x4 pq = ph32 + __builtin_convertvector(pl, f32x4);
+        l = l * alpha + ((pq[0] + pq[1]) + (pq[2] + pq[3]));
         m = mnew;
 
         // V^T operands in registers: tile t row c is dim 8c + t, its k index
@@ -516,12 +521,18 @@ __device__ inline void wave_attend(const AttnParams& p, const WaveSeg& cs, const
 #pragma unroll
             for (int t = 0; t < 8; ++t) acc[t] *= alpha;
         }
-        // O^T += V^T P^T, eight 16-dim tiles
+        // O^T += V^T P^T, eight 16-dim tiles, the high parts of P, then the
+        // low parts (independent accumulators between the two passes)
+        typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
-            typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
             const u32x2 av = {a[t][0], a[t][1]};
             acc[t] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, av), ph, acc[t], 0, 0, 0);
+        }
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const u32x2 av = {a[t][0], a[t][1]};
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, av), pl, acc[t], 0, 0, 0);
         }
     };
 
@@ -563,12 +574,12 @@ __device__ inline void write_row(const AttnParams& p, int b, int head, int dim, 
 
 // Folds the current token (logit sn in log2 units, value vn) into a merged
 // state: running max M (log2 units; -inf when empty) and num, den relative
-// to it.  The weight is rounded to fp16 like the cached tokens' weights.
+// to it, with its fp32 weight.
 __device__ inline void fold_new_token(float sn, float vn, float& M, float& num, float& den)
 {
     const float M2 = fmaxf(M, sn);
     const float r = M == -INFINITY ? 0.f : exp2_fast(M - M2);
-    const float wgt = (float)(f16)exp2_fast(sn - M2);
+    const float wgt = exp2_fast(sn - M2);
     num = fmaf(wgt, vn, num * r);
     den = fmaf(den, r, wgt);
     M = M2;

@@ -460,3 +460,43 @@ def test_random_configurations(torch_cuda, apex, oracle_mod, seed):
     assert np.all(got[np.asarray(lens) == 0] == 0)
     if kw.get("check_inputs"):
         assert apex.check_device_error() == 0
+
+
+# ---------------------------------------------------------------------------
+# precision: with fp32 scores and accumulation and the softmax weights carried
+# as two fp16 MFMA operands (22 significant bits), the GPU's value before the
+# final rounding is off by about 1e-6 absolute (fp32 sums of weighted N(0, 1)
+# values), far below an fp16 spacing at every output magnitude above ~2^-10,
+# so every output is one of the two fp16 neighbours of the exact (fp64) value
+# up to that allowance, and nearly always the nearest one: only values within
+# it of a rounding midpoint can go the other way (a bias would show as ~50 %)
+# ---------------------------------------------------------------------------
+
+FP32_ALLOWANCE = 1e-6
+
+
+def fp16_ulp(x):
+    """Spacing of fp16 values at |x| (the subnormal spacing below 2^-14)."""
+    e = np.floor(np.log2(np.maximum(np.abs(x), 2.0 ** -14)))
+    return 2.0 ** (e - 10)
+
+
+@pytest.mark.parametrize("name,lens,Hq,Hkv", SMALL + [("few_tokens", [1, 2, 3, 2, 5, 2, 17], 32, 8)],
+                         ids=[s[0] for s in SMALL] + ["few_tokens"])
+@pytest.mark.parametrize("workers", [0, 7])
+def test_outputs_are_fp16_neighbours_of_the_exact_result(torch_cuda, apex, oracle_mod, name, lens, Hq, Hkv,
+                                                         workers):
+    case = W.make_host_case(lens, Hq, Hkv, seed=len(lens) * 13 + Hq, poison=True)
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale)
+    got = run_gpu(torch_cuda, apex, case, num_workers=workers).astype(np.float64)
+    nonzero = np.asarray(lens) > 0
+    ref, got = ref[nonzero], got[nonzero]
+    excess = np.abs(got - ref) - fp16_ulp(ref)
+    worst = int(np.argmax(excess))
+    print(f"[precision] {name} workers={workers}: max excess over one fp16 spacing {excess.flat[worst]:.2e} "
+          f"at exact value {ref.flat[worst]:.3e}", flush=True)
+    assert np.all(excess <= FP32_ALLOWANCE), "an output is not an fp16 neighbour of the exact value"
+    nearest = got == ref.astype(np.float16).astype(np.float64)
+    print(f"[precision] {name} workers={workers}: {nearest.mean():.6f} of outputs correctly rounded", flush=True)
+    assert nearest.mean() >= 0.98
