@@ -8,7 +8,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libapex_decode.so")
-SOURCES = [os.path.join(CSRC, "apex_decode.hip"), os.path.join(CSRC, "kv_append.hip")]
+SOURCES = [os.path.join(CSRC, "apex_decode.hip"), os.path.join(CSRC, "kv_append.hip"),
+           os.path.join(CSRC, "plan_host.cpp"), os.path.join(CSRC, "status.cpp")]
 CPU_LIB = os.path.join(HERE, "libapex_cpu.so")
 CPU_DIR = os.path.join(CSRC, "cpu")
 OVERLAP_LIB = os.path.join(HERE, "libapex_overlap.so")

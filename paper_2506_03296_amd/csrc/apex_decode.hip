@@ -20,27 +20,6 @@
 #include "plan_policy.h"
 #include "status.h"
 
-namespace apex {
-
-namespace {
-thread_local char g_last_error[512] = "";
-}
-
-int fail(int code, const char* fmt, ...)
-{
-    va_list ap;
-    va_start(ap, fmt);
-    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
-    va_end(ap);
-    return code;
-}
-
-void clear_error() { g_last_error[0] = 0; }
-
-const char* last_error_message() { return g_last_error; }
-
-}  // namespace apex
-
 namespace {
 
 // Static scratch of apex_decode_attention_noalloc: arrival counters for up to
@@ -461,49 +440,6 @@ size_t apex_decode_workspace_bytes(int B, int Hq, int Hkv, int d, int block_size
             return 0;
     }
     return counter_bytes(B, Hkv) + partial_bytes(workers, Hq / Hkv);
-}
-
-int apex_decode_plan_host(const int32_t* context_lens, int B, int Hkv, int block_size,
-                          int launched_workers, int forced, int cus, int32_t* contributors_out,
-                          int64_t* units_out, int64_t* active_out, int64_t* partials_out)
-{
-    apex::clear_error();
-    if (B < 0 || Hkv <= 0 || launched_workers <= 0 || cus < 0)
-        return fail(APEX_ERR_INVALID_ARG, "bad partition arguments");
-    if (B > 0 && !context_lens) return fail(APEX_ERR_INVALID_ARG, "context_lens is NULL");
-    if (block_size != apex::kBlockSize)
-        return fail(APEX_ERR_UNSUPPORTED, "block_size %d unsupported (only 16)", block_size);
-    int64_t blocks = 0, nonempty = 0;
-    for (int b = 0; b < B; ++b) {
-        blocks += apex::blocks_of(context_lens[b], block_size);
-        nonempty += context_lens[b] > 0;
-    }
-    const int64_t units = blocks * Hkv;
-    const int64_t pairs = nonempty * Hkv;
-    const int64_t W = apex::active_workers(units, launched_workers,
-                                           forced ? 1 : apex::kMinUnitsPerWorker, pairs,
-                                           forced ? 0 : cus);
-    const int64_t K = forced ? 0 : apex::kSegmentCostUnits;
-    const int64_t V = units + K * pairs;
-    int64_t partials = 0, pre = 0, pp = 0;
-    for (int b = 0; b < B; ++b) {
-        const int64_t nb = apex::blocks_of(context_lens[b], block_size);
-        for (int g = 0; g < Hkv; ++g) {
-            int64_t n = 0;
-            if (nb > 0) {
-                const int64_t vf = apex::first_block_position(pre * Hkv + (int64_t)g * nb, pp * Hkv + g, K);
-                n = apex::worker_of(vf + nb - 1, V, W) - apex::worker_of(vf, V, W) + 1;
-                if (n > 1) partials += n;
-            }
-            if (contributors_out) contributors_out[(size_t)b * Hkv + g] = (int32_t)n;
-        }
-        pre += nb;
-        pp += nb > 0;
-    }
-    if (units_out) *units_out = units;
-    if (active_out) *active_out = units > 0 ? W : 0;
-    if (partials_out) *partials_out = partials;
-    return APEX_OK;
 }
 
 int apex_decode_attention_ex(const apex_decode_args* args)
