@@ -3,9 +3,10 @@
     python bench.py [--steps K] [--warmup W] [--workload c4]
 
 A step is one apex_decode_attention call (one persistent kernel that plans,
-attends and combines) over the whole batch with inputs resident in HBM.  W untimed steps,
-then K steps back to back between two device synchronisations.  Prints one
-JSON line:
+attends and combines) over the whole batch with inputs resident in HBM.  Whole
+steps for --prewarm-ms (200 ms: the GPU reaches its steady clocks; calls after
+an idle spell run up to 3-4 % slower), then W untimed steps, then K steps back
+to back between two device synchronisations.  Prints one JSON line:
 
   value      algorithmic HBM GB/s of the whole step: (KV + Q + O bytes of valid
              tokens) / (ms per step); us_per_layer_step alongside
@@ -487,16 +488,25 @@ def measure_fused_step(A, torch, wl, steps=50, warmup=20):
                       "before and one after the fused run"}
 
 
-def time_workload(A, torch, wl, steps, warmup, workers=0):
-    """The timings of one workload: W untimed steps, K steps back to back
-    between two synchronisations (whole step), K steps with events recorded by
-    the library around the kernel (kernel alone), and COLD_REPS calls each
-    after a 512 MiB read (cold caches).  Returns the figures and a host copy
-    of the output of the last back-to-back step."""
+def time_workload(A, torch, wl, steps, warmup, workers=0, prewarm_ms=0.0):
+    """The timings of one workload: whole steps for prewarm_ms (the GPU at its
+    steady clocks: calls after an idle spell run up to 3-4 % slower), W
+    untimed steps, K steps back to back between two synchronisations (whole
+    step), K steps with events recorded by the library around the kernel
+    (kernel alone), and COLD_REPS calls each after a 512 MiB read (cold
+    caches).  Returns the figures and a host copy of the output of the last
+    back-to-back step."""
     def step(events=None):
         A.decode_attention_ex(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens,
                               wl.scale, out=wl.out, num_workers=workers, events=events)
 
+    prewarm_calls = 0
+    t_end = time.perf_counter() + prewarm_ms * 1e-3
+    while time.perf_counter() < t_end:
+        for _ in range(10):
+            step()
+        prewarm_calls += 10
+        torch.cuda.synchronize()
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
@@ -538,7 +548,7 @@ def time_workload(A, torch, wl, steps, warmup, workers=0):
     cold_ms = sorted(a.elapsed_time(b) for a, b in cold_pairs)
     del scratch
     return {"ms_per_step": ms_per_step, "wall_s_per_step": wall / steps, "kern_ms": kern_ms,
-            "cold_ms": cold_ms}, timed_out
+            "cold_ms": cold_ms, "prewarm_calls": prewarm_calls}, timed_out
 
 
 def workload_line(wl, t, traffic):
@@ -566,7 +576,7 @@ def workload_line(wl, t, traffic):
     }
 
 
-def measure_workloads(A, torch, W, names, steps, warmup, workers, done):
+def measure_workloads(A, torch, W, names, steps, warmup, workers, done, prewarm_ms):
     """The other named workloads, each generated, timed like the headline one
     and freed in turn (``done`` holds lines already measured)."""
     lines = dict(done)
@@ -576,7 +586,7 @@ def measure_workloads(A, torch, W, names, steps, warmup, workers, done):
         log(f"workload {name}: generating")
         wl = W.DeviceWorkload(name)
         torch.cuda.synchronize()
-        t, _ = time_workload(A, torch, wl, steps, warmup, workers)
+        t, _ = time_workload(A, torch, wl, steps, warmup, workers, prewarm_ms)
         lines[name] = workload_line(wl, t, committed_traffic(name))
         if name == "c1":
             lines[name]["kind"] = "latency (13 MB: the batch fits in the caches)"
@@ -600,6 +610,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=500,
                     help="untimed steps first; ~0.1 s of continuous calls brings the GPU to its "
                          "steady clocks (the first calls after idle run up to 3-4 %% slower)")
+    ap.add_argument("--prewarm-ms", type=float, default=200.0,
+                    help="whole steps for this long before the warmup steps, so the GPU is at its "
+                         "steady clocks when the warmup steps begin (0 = none)")
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -668,7 +681,7 @@ def main():
     torch.cuda.synchronize()
 
     log(f"warmup {args.warmup}, timing {args.steps} steps")
-    t, timed_out = time_workload(A, torch, wl, args.steps, args.warmup, args.workers)
+    t, timed_out = time_workload(A, torch, wl, args.steps, args.warmup, args.workers, args.prewarm_ms)
     ms_per_step = t["ms_per_step"]
     kern_ms = t["kern_ms"]
     kern_mean = sum(kern_ms) / len(kern_ms)
@@ -685,6 +698,8 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "prewarm": {"ms": args.prewarm_ms, "calls": t["prewarm_calls"],
+                    "what": "whole steps before the W warmup steps, until the GPU is at its steady clocks"},
         "ms_per_step": round(ms_per_step, 5),
         "us_per_layer_step": round(ms_per_step * 1e3, 2),
         "pct_of_peak_hbm": round(100.0 * nbytes / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 2),
@@ -744,7 +759,8 @@ def main():
         del wl
         torch.cuda.empty_cache()
         result["workloads"] = measure_workloads(A, torch, W, WORKLOADS, args.steps, args.warmup,
-                                                args.workers, {args.workload: headline_line})
+                                                args.workers, {args.workload: headline_line},
+                                                args.prewarm_ms)
     print(json.dumps(result), flush=True)
     if result["parity"] is not None and not result["parity"]["ok"]:
         print("bench.py: the timed output fails the parity bar against the oracle", file=sys.stderr)
