@@ -291,3 +291,28 @@ def test_fused_append_checked_path_context_past_its_row(torch_cuda, apex, oracle
     assert np.array_equal(got_k[last, :, 15].view(np.uint16), kc[last, :, 15].view(np.uint16))
     assert np.array_equal(got_k.view(np.uint16), exp_k.view(np.uint16))
     assert np.array_equal(got_v.view(np.uint16), exp_v.view(np.uint16))
+
+
+def test_fused_append_when_every_context_is_only_its_current_token_or_empty(torch_cuda, apex, oracle_mod):
+    """Nothing cached at all: every request's output is its new V row (one
+    token) or zeros (empty), and the new rows land in their slots."""
+    torch = torch_cuda
+    lens = [1, 0, 1, 1, 0]
+    case, kc, vc, kn, vn, exp_k, exp_v = fused_case(lens, 4, 8, seed=171)
+    dev = "cuda"
+    kd, vd = torch.from_numpy(kc).to(dev), torch.from_numpy(vc).to(dev)
+    for workers in (0, 2):
+        out = apex.decode_attention_ex(torch.from_numpy(case.q).to(dev), kd, vd,
+                                       torch.from_numpy(case.block_table).to(dev),
+                                       torch.from_numpy(case.context_lens).to(dev), case.scale,
+                                       num_workers=workers, k_new=torch.from_numpy(kn).to(dev),
+                                       v_new=torch.from_numpy(vn).to(dev))
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        for b, L in enumerate(lens):
+            if L == 1:
+                assert np.array_equal(got[b].view(np.uint16), np.repeat(vn[b], 4, axis=0).view(np.uint16))
+            else:
+                assert np.all(got[b] == 0)
+        assert np.array_equal(kd.cpu().numpy().view(np.uint16), exp_k.view(np.uint16))
+        assert np.array_equal(vd.cpu().numpy().view(np.uint16), exp_v.view(np.uint16))

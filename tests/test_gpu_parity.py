@@ -500,3 +500,38 @@ def test_outputs_are_fp16_neighbours_of_the_exact_result(torch_cuda, apex, oracl
     nearest = got == ref.astype(np.float16).astype(np.float64)
     print(f"[precision] {name} workers={workers}: {nearest.mean():.6f} of outputs correctly rounded", flush=True)
     assert nearest.mean() >= 0.98
+
+
+# ---------------------------------------------------------------------------
+# degenerate batches: nothing to attend, or one request among many empty ones
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("lens", [[0], [0, 0, -3, 0], [-1] * 300], ids=["one", "four", "300"])
+def test_all_empty_batch_gives_zero_rows(torch_cuda, apex, lens):
+    torch = torch_cuda
+    case = W.make_host_case(lens, 32, 8, seed=41, poison=True)
+    q, k, v, bt, cl = to_dev(torch, case)
+    B = len(lens)
+    for kw in (dict(), dict(num_workers=5), dict(check_inputs=True)):
+        lse = torch.zeros((B, 32), dtype=torch.float32, device="cuda")
+        out = torch.full((B, 32, 128), 7.0, dtype=torch.float16, device="cuda")
+        apex.decode_attention_ex(q, k, v, bt, cl, case.scale, out=out, lse_out=lse, **kw)
+        torch.cuda.synchronize()
+        assert bool((out == 0).all()), kw
+        assert bool(torch.isneginf(lse).all()), kw
+    assert apex.check_device_error() == 0
+    out = torch.full((B, 32, 128), 7.0, dtype=torch.float16, device="cuda")
+    apex.decode_attention_noalloc(q, k, v, bt, cl, case.scale, out)
+    torch.cuda.synchronize()
+    assert bool((out == 0).all())
+
+
+def test_one_long_request_among_many_empty_ones(torch_cuda, apex, oracle_mod):
+    lens = [0] * 150 + [5000] + [0, 1] * 60 + [0] * 80
+    case = W.make_host_case(lens, 32, 8, seed=42, poison=True)
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale)
+    for workers in (0, 3, 100):
+        got = run_gpu(torch_cuda, apex, case, num_workers=workers)
+        assert_parity(got, ref, f"one long among empty, workers={workers}")
+        assert np.all(got[np.asarray(lens) == 0] == 0)
