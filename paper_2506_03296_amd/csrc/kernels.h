@@ -9,14 +9,16 @@
 //      its own (block sums, a prefix scan, the longest request for the tight
 //      block-table stride), so no planner kernel runs before it;
 //   2. walks its contiguous range of (request b, kv-head g, block) units
-//      segment by segment.  In a segment the four waves take the blocks of
-//      one (b, g) pair round-robin; per 16-token block a wave gathers the
-//      paged K/V rows with 128-bit loads (two blocks in flight per wave),
-//      computes the G q-heads' scores as S^T = K Q^T with four
-//      16x16x32 fp16 MFMAs (q-heads padded to 16 columns), runs an online
-//      softmax (running max and sum in base 2, log2(e) folded into the
-//      scale), and accumulates O^T += V^T P^T in fp32 with eight 16x16x16
-//      fp16 MFMAs, V^T being assembled in registers with byte permutes.
+//      (ranges of equal cost, a pair's cost being its blocks plus a fixed
+//      start-up charge) segment by segment.  In a segment the four waves
+//      take the blocks of one (b, g) pair round-robin; per 16-token block a
+//      wave gathers the paged K/V rows with 128-bit loads (two blocks in
+//      flight per wave), computes the G q-heads' scores as S^T = K Q^T with
+//      four 16x16x32 fp16 MFMAs (q-heads padded to 16 columns), runs an
+//      online softmax (running max and sum in base 2, log2(e) folded into
+//      the scale), and accumulates O^T += V^T P^T in fp32 with sixteen
+//      16x16x16 fp16 MFMAs -- the weights P as two fp16 parts, 22 bits --
+//      V^T being assembled in registers with byte permutes.
 //      Each wave's K/V pipeline runs on across segments: between two long
 //      segments the last steps of one already load the next one's first
 //      blocks, and the next segment's Q operand is loaded one segment ahead;
