@@ -312,6 +312,13 @@ def test_one_long_request_split_over_many_work_groups(torch_cuda, apex, oracle_m
     got = run_gpu(torch, apex, case, num_workers=768, lse_out=lse)
     assert_parity(got, ref, "L=65536")
     assert np.max(np.abs(lse.cpu().numpy() - lse_ref)) < 1e-4
+    # the default grid (equal-cost ranges, one work group per CU here): 32
+    # contributors per pair, combined in four chunks
+    plan = apex.plan_host(case.context_lens, 8, 512, cus=256)
+    assert plan["contributors"].min() > 8
+    got = run_gpu(torch, apex, case, lse_out=lse)
+    assert_parity(got, ref, "L=65536, default grid")
+    assert np.max(np.abs(lse.cpu().numpy() - lse_ref)) < 1e-4
 
 
 # ---------------------------------------------------------------------------

@@ -121,3 +121,50 @@ def test_noalloc_refuses_more_pairs_than_its_scratch(torch_cuda, apex):
     assert "65536" in str(e.value)
     torch.cuda.synchronize()
     assert bool((out == 7.0).all())
+
+
+def test_noalloc_captured_in_a_graph_and_replayed(torch_cuda, apex):
+    """The no-allocation call captured in a HIP graph (torch.cuda.graph) and
+    replayed; between replays, eager work and eager no-allocation calls of
+    another batch share the static scratch.  Every replay must equal the base
+    call bit for bit, and a replay must see an in-place change of the query."""
+    torch = torch_cuda
+    dev = "cuda"
+    case = W.make_host_case([3000, 17, 900, 4500, 0, 1, 2048], 32, 8, seed=81, poison=True)
+    q, k, v = (torch.from_numpy(x).to(dev) for x in (case.q, case.k_cache, case.v_cache))
+    bt, cl = torch.from_numpy(case.block_table).to(dev), torch.from_numpy(case.context_lens).to(dev)
+    other = W.make_host_case([700, 33, 5000], 16, 4, seed=82, poison=True)
+    oq, ok_, ov = (torch.from_numpy(x).to(dev) for x in (other.q, other.k_cache, other.v_cache))
+    obt, ocl = torch.from_numpy(other.block_table).to(dev), torch.from_numpy(other.context_lens).to(dev)
+    ref = apex.decode_attention(q, k, v, bt, cl, case.scale)
+    oref = apex.decode_attention(oq, ok_, ov, obt, ocl, other.scale)
+    out = torch.empty_like(q)
+    oout = torch.empty_like(oq)
+
+    # warm up on a side stream (the device's first call sets up outside the capture)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        apex.decode_attention_noalloc(q, k, v, bt, cl, case.scale, out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
+
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        apex.decode_attention_noalloc(q, k, v, bt, cl, case.scale, out)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        out.fill_(7.0)
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), ref.view(torch.int16)), f"replay {rep}"
+        apex.decode_attention_noalloc(oq, ok_, ov, obt, ocl, other.scale, oout)   # another batch
+        torch.cuda.synchronize()
+        assert torch.equal(oout.view(torch.int16), oref.view(torch.int16)), f"eager call after replay {rep}"
+
+    q.mul_(-0.5)
+    ref2 = apex.decode_attention(q, k, v, bt, cl, case.scale)
+    graph.replay()
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), ref2.view(torch.int16)), "replay after a new query"
