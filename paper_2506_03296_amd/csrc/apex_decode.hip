@@ -394,6 +394,7 @@ int enqueue(const apex_decode_args& a, bool noalloc)
     p.min_units = a.num_workers > 0 ? 1 : apex::kMinUnitsPerWorker;
     p.seg_cost = a.num_workers > 0 ? 0 : apex::kSegmentCostUnits;
     p.cus = cus;
+    p.launched = (int)workers;
     p.num_blocks = check ? a.num_blocks : 0;
     p.error_word = (unsigned*)error_word;
     p.k_new = (const apex::f16*)a.k_new;

@@ -68,6 +68,7 @@ struct AttnParams {
     int min_units;         // minimum units per active worker
     int seg_cost;          // cost positions charged per pair (plan_policy.h), 0 = equal units
     int cus;               // compute units for the one-group-per-CU rule (0 = off)
+    int launched;          // work groups launched (the grid size)
     int64_t num_blocks;    // physical blocks in the caches (input check only)
     unsigned* error_word;  // input-check error bits (input check only)
     // Fused append (optional): the current token's K/V rows, [B][Hkv][D] with
@@ -698,12 +699,32 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     const int64_t units = (int64_t)uniform(total) * p.Hkv;
     const int64_t pairs = (int64_t)uniform(nonempty) * p.Hkv;
     const int64_t stride = p.bt_stride > 0 ? p.bt_stride : (int64_t)uniform(maxb);
-    const int64_t W = active_workers(units, (int64_t)gridDim.x, p.min_units, pairs, p.cus);
     // the cost line: every non-empty pair's K cost positions, then its blocks
     const int64_t K = p.seg_cost;
     const int64_t V = units + K * pairs;
-    const int64_t v0 = units > 0 && w < W ? worker_start(w, V, W) : 0;
-    const int64_t v1 = units > 0 && w < W ? worker_start(w + 1, V, W) : 0;
+    // The prologue is serial code of one wave per work group, so its time is
+    // its instruction count: when V (launched + 1) < 2^32 (any batch below
+    // about 8 M units at the default grid) every product below fits 32 bits
+    // and the partition runs in 32-bit arithmetic, else in 64-bit; both give
+    // the same ranges.  Lanes 0 and 1 find the range's two ends in one
+    // division.
+    const bool narrow = ((uint64_t)V >> 32) == 0 && (uint64_t)V * ((uint64_t)p.launched + 1) <= 0xffffffffull;
+    int64_t W, v0, v1;
+    if (narrow) {
+        const uint32_t W32 = active_workers_t<uint32_t>((uint32_t)units, (uint32_t)p.launched, (uint32_t)p.min_units,
+                                                        (uint32_t)pairs, (uint32_t)p.cus);
+        const uint32_t ends = units > 0 && w < W32 ? (uint32_t)(w + (lane & 1)) * (uint32_t)V / W32 : 0u;
+        W = W32;
+        v0 = (uint32_t)__builtin_amdgcn_readlane((int)ends, 0);
+        v1 = (uint32_t)__builtin_amdgcn_readlane((int)ends, 1);
+    } else {
+        W = active_workers(units, (int64_t)p.launched, p.min_units, pairs, p.cus);
+        const int64_t ends = units > 0 && w < W ? worker_start(w + (lane & 1), V, W) : 0;
+        v0 = ((int64_t)__builtin_amdgcn_readlane((int)(ends >> 32), 0) << 32) |
+             (uint32_t)__builtin_amdgcn_readlane((int)ends, 0);
+        v1 = ((int64_t)__builtin_amdgcn_readlane((int)(ends >> 32), 1) << 32) |
+             (uint32_t)__builtin_amdgcn_readlane((int)ends, 1);
+    }
 
     // The worker's blocks are those whose positions lie in [v0, v1).  Request
     // b's positions start at Hkv (pre_b + K pp_b) (pre_b blocks and pp_b
@@ -711,30 +732,39 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
     // whose requests hold v0 finds the pair there and its first block at or
     // after v0 (block 0 when v0 is one of the pair's cost positions), and
     // publishes the pair, that block and the position of the pair's block 0.
-    if (v0 < v1) {
-        const int64_t hk = p.Hkv;
-        const int64_t lo = (int64_t)(incl - tsum) + K * (incl_cnt - own_cnt);
-        const int64_t hi = (int64_t)incl + K * incl_cnt;
-        if (lo * hk <= v0 && v0 < hi * hk) {
-            int64_t pre = incl - tsum, vpre = lo * hk;
+    // (In I = uint32_t every position is below V < 2^32.)
+    auto locate = [&](auto at) {
+        using I = decltype(at);
+        const I hk = (I)p.Hkv, Kc = (I)K;
+        const I lo = (I)(incl - tsum) + Kc * (I)(incl_cnt - own_cnt);
+        const I hi = (I)incl + Kc * (I)incl_cnt;
+        if (lo * hk <= at && at < hi * hk) {
+            I pre = (I)(incl - tsum), vpre = lo * hk;
             for (int b = r0; b < r1; ++b) {
-                const int nb = (int)blocks_of(len_of(b), kBlockSize);
+                // with one request per thread, its block count is the scan's
+                const I nb = seg == 1 ? (I)tsum : (I)blocks_of(len_of(b), kBlockSize);
                 if (nb == 0) continue;
-                const int64_t span = (int64_t)(nb + K) * hk;
-                if (v0 < vpre + span) {
-                    const int64_t g = div_floor(v0 - vpre, nb + K);
-                    const int64_t vf = vpre + g * (nb + K) + K;   // position of the pair's block 0
+                const I span = (nb + Kc) * hk;
+                if (at < vpre + span) {
+                    const I g = div_floor(at - vpre, nb + Kc);
+                    const I vf = vpre + g * (nb + Kc) + Kc;   // position of the pair's block 0
                     s_loc_b = b;
-                    s_loc_pre = pre;
+                    s_loc_pre = (int64_t)pre;
                     s_loc_g = (int)g;
-                    s_loc_blk = (int)(v0 > vf ? v0 - vf : 0);
-                    s_loc_vf = vf;
+                    s_loc_blk = (int)(at > vf ? at - vf : 0);
+                    s_loc_vf = (int64_t)vf;
                     break;
                 }
                 pre += nb;
                 vpre += span;
             }
         }
+    };
+    if (v0 < v1) {
+        if (narrow)
+            locate((uint32_t)v0);
+        else
+            locate(v0);
     }
     __syncthreads();
 

@@ -39,12 +39,22 @@ constexpr int kSegmentCostUnits = 8;
 
 // floor(a / b) for a >= 0, b > 0.  A 64-bit division is a long software
 // sequence on the GPU; the partition's operands nearly always fit in 32 bits,
-// where the hardware-assisted 32-bit sequence gives the same quotient.
-__host__ __device__ inline int64_t div_floor(int64_t a, int64_t b)
+// where the hardware-assisted 32-bit sequence gives the same quotient.  The
+// 64-bit one is kept out of line, so that the code a work group runs before
+// its first load stays short.
+__host__ __device__ __attribute__((noinline)) inline int64_t div_floor_wide(int64_t a, int64_t b)
 {
-    if (((uint64_t)a | (uint64_t)b) <= 0xffffffffull) return (int64_t)((uint32_t)a / (uint32_t)b);
     return a / b;
 }
+
+__host__ __device__ inline int64_t div_floor(int64_t a, int64_t b)
+{
+    if (__builtin_expect(((uint64_t)a | (uint64_t)b) <= 0xffffffffull, 1))
+        return (int64_t)((uint32_t)a / (uint32_t)b);
+    return div_floor_wide(a, b);
+}
+
+__host__ __device__ inline uint32_t div_floor(uint32_t a, uint32_t b) { return a / b; }
 
 __host__ __device__ inline int64_t blocks_of(int32_t len, int bs)
 {
@@ -60,14 +70,22 @@ __host__ __device__ inline int64_t blocks_of(int32_t len, int bs)
 // work groups: one per CU (work groups are handed out round-robin over the
 // XCDs and then over their CUs), no pair split between two groups, and no
 // second group sharing the CU.
-__host__ __device__ inline int64_t active_workers(int64_t units, int64_t launched, int min_units,
-                                                  int64_t pairs, int64_t cus)
+// The integer type I is int64_t, or uint32_t where the caller has shown that
+// every operand and cus * kUnitsPerCuForOne fit (the kernel's 32-bit path).
+template <typename I>
+__host__ __device__ inline I active_workers_t(I units, I launched, I min_units, I pairs, I cus)
 {
-    if (cus > 0 && pairs <= cus && units <= cus * kUnitsPerCuForOne && launched > cus) launched = cus;
-    int64_t w = div_floor(units, min_units > 0 ? min_units : 1);
+    if (cus > 0 && pairs <= cus && units <= cus * (I)kUnitsPerCuForOne && launched > cus) launched = cus;
+    I w = div_floor(units, min_units > 0 ? min_units : (I)1);
     if (w < pairs) w = pairs;
     if (w < 1) w = 1;
     return w < launched ? w : launched;
+}
+
+__host__ __device__ inline int64_t active_workers(int64_t units, int64_t launched, int min_units,
+                                                  int64_t pairs, int64_t cus)
+{
+    return active_workers_t<int64_t>(units, launched, min_units, pairs, cus);
 }
 
 // First position of worker w on the cost line of `positions` positions (the

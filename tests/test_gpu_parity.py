@@ -322,6 +322,54 @@ def test_one_long_request_split_over_many_work_groups(torch_cuda, apex, oracle_m
 
 
 # ---------------------------------------------------------------------------
+# the partition's 32-bit and 64-bit arithmetic.  The kernel partitions in 32
+# bits when V (launched + 1) < 2^32 (V = units on a forced grid) and in 64
+# bits otherwise; forced grids of up to 2^17 work groups put cases on both
+# sides of that bound, and past 2^32 in the range-end products.  The table
+# entries repeat blocks of a small pool, so a large unit count takes little
+# memory.
+# ---------------------------------------------------------------------------
+
+def shared_pool_case(B, L, Hq, Hkv, pool, seed):
+    rng = np.random.default_rng(seed)
+    nb = -(-L // W.BLOCK_SIZE)
+    q = rng.standard_normal((B, Hq, W.D_HEAD)).astype(np.float16)
+    k = rng.standard_normal((pool, Hkv, W.BLOCK_SIZE, W.D_HEAD)).astype(np.float16)
+    v = rng.standard_normal((pool, Hkv, W.BLOCK_SIZE, W.D_HEAD)).astype(np.float16)
+    table = rng.integers(0, pool, size=(B, nb), dtype=np.int32)
+    return W.HostCase(q, k, v, table, np.full(B, L, dtype=np.int32), W.SCALE)
+
+
+def test_partition_64_bit_path_with_range_products_past_2_32(torch_cuda, apex, oracle_mod):
+    # 8 requests x 8 kv-heads x 2048 blocks = 2^17 units on 2^17 work groups:
+    # V (launched + 1) ~ 2^34, and w V reaches ~2^34; 2048 contributors per pair
+    case = shared_pool_case(8, 2048 * 16 - 5, 8, 8, 1024, seed=171)
+    units = 8 * 8 * 2048
+    assert units * (units + 1) > 2**32
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale)
+    got = run_gpu(torch_cuda, apex, case, num_workers=units)
+    assert_parity(got, ref, "2^17 units on 2^17 work groups (64-bit partition)")
+
+
+def test_partition_32_and_64_bit_paths_agree_at_the_bound(torch_cuda, apex, oracle_mod):
+    # 255 requests x 257 blocks = 65535 units (one kv-head): on 65536 work
+    # groups V (launched + 1) = 2^32 - 1, the largest 32-bit case; on 65537 it
+    # is 2^32 + 65534 (64-bit).  Both use 65535 workers, so their ranges, and
+    # hence their outputs, must be the same bit for bit.
+    case = shared_pool_case(255, 257 * 16 - 3, 1, 1, 1024, seed=172)
+    units = 255 * 257
+    assert units * (65536 + 1) == 2**32 - 1 and units * (65537 + 1) > 2**32 - 1
+    ref = oracle_mod.decode_attention_f64(case.q, case.k_cache, case.v_cache, case.block_table,
+                                          case.context_lens, case.scale)
+    narrow = run_gpu(torch_cuda, apex, case, num_workers=65536)
+    wide = run_gpu(torch_cuda, apex, case, num_workers=65537)
+    assert_parity(narrow, ref, "65535 units, 32-bit partition")
+    assert_parity(wide, ref, "65535 units, 64-bit partition")
+    assert np.array_equal(narrow.view(np.uint16), wide.view(np.uint16))
+
+
+# ---------------------------------------------------------------------------
 # input check (APEX_DECODE_FLAG_CHECK_INPUTS)
 # ---------------------------------------------------------------------------
 
