@@ -16,7 +16,8 @@ to back between two device synchronisations.  Prints one JSON line:
              HBM bytes per launch from the committed rocprofv3 counter summary
              when it was taken on the current kernel source, else null
   cpu_baseline  the fp64 CPU oracle on the host cores over a bounded sample of
-             the same workload (the first requests), in the same unit
+             the same workload (the first requests), in the same unit; its
+             single_thread entry is the same on one thread (about 2 s)
   cpu_attention  the library's own host backend (libapex_cpu.so, SIMD +
              thread pool) on a host copy of the same workload, against the
              host read bandwidth measured with the same threads
@@ -51,7 +52,9 @@ to back between two device synchronisations.  Prints one JSON line:
              whole step, kernel alone (events) and kernel with cold caches,
              algorithmic GB/s and fraction of the HBM peak, and the committed
              counter traffic when it matches the kernel source (c1, 13 MB,
-             fits in the caches: a latency figure)
+             fits in the caches: a latency figure); with the CPU baseline on,
+             each also carries cpu_baseline_1_thread, the fp64 oracle on one
+             host thread over a sample of that workload (about 2 s)
 Inside roofline, kernel_us_cold_median / achieved_cold time the kernel after
 a 512 MiB read has evicted the caches (the figure that relies on no K/V left
 in a cache by the previous call).
@@ -75,6 +78,7 @@ if ROOT not in sys.path:
 METRIC = "decode-attn µs/layer-step + achieved HBM GB/s (% peak), Llama-3.1-8B GQA"
 PEAK_HBM_GBS = 8000.0
 COLD_REPS = 20        # calls timed after evicting the caches
+SINGLE_THREAD_SECONDS = 2.0   # the one-thread oracle sample of each workload
 PARITY_MAX_ABS = 2e-3  # the attention bar: fp16 output, fp32 accumulation
 PARITY_REL_L2 = 1e-3
 WORKLOADS = ("c1", "c2", "c3", "c4", "c5")
@@ -123,18 +127,15 @@ def committed_traffic(workload):
     return entry.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(wl, target_s, timed_out=None):
-    """Time the fp64 oracle on the host over the first requests of the batch.
-
-    With ``timed_out`` (host copy of the output of the last timed step) the
-    oracle's result over those requests is also compared with it: the parity
-    of what the benchmark timed, against the attention bar (max-abs <= 2e-3,
-    relative L2 <= 1e-3, all finite)."""
+def oracle_rate(wl, threads, target_s):
+    """The fp64 oracle on `threads` host threads over the first requests of
+    the batch: one request first, then as many as take about target_s (at
+    most the whole batch).  Returns the rate line, the host case and the
+    oracle's output."""
     import numpy as np
 
     import oracle
     import apex_workloads as W
-    threads = max(1, min(16, len(os.sched_getaffinity(0))))
     cfg = wl.cfg
 
     def run(n):
@@ -146,12 +147,12 @@ def cpu_baseline(wl, target_s, timed_out=None):
 
     n = 1
     dt, case, ref = run(n)
-    if dt < target_s:
+    if dt < target_s and n < cfg.B:
         per = dt / n
         n = int(min(cfg.B, max(1, target_s / max(per, 1e-6))))
         dt, case, ref = run(n)
     nbytes = W.algorithmic_bytes(case.context_lens, n, cfg.Hq, cfg.Hkv, cfg.d)
-    baseline = {
+    line = {
         "value": round(nbytes / dt / 1e9, 4),
         "unit": "GB/s",
         "cores": threads,
@@ -159,6 +160,23 @@ def cpu_baseline(wl, target_s, timed_out=None):
         "sample": f"first {n} of {cfg.B} requests ({int(np.sum(case.context_lens))} tokens, "
                   f"{nbytes / 1e6:.1f} MB algorithmic), fp64 plain-loop oracle, {dt:.2f} s",
     }
+    return line, case, ref, n
+
+
+def cpu_baseline(wl, target_s, timed_out=None):
+    """Time the fp64 oracle on the host over the first requests of the batch,
+    on up to 16 threads and on one.
+
+    With ``timed_out`` (host copy of the output of the last timed step) the
+    oracle's result over those requests is also compared with it: the parity
+    of what the benchmark timed, against the attention bar (max-abs <= 2e-3,
+    relative L2 <= 1e-3, all finite)."""
+    import numpy as np
+
+    cfg = wl.cfg
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    baseline, case, ref, n = oracle_rate(wl, threads, target_s)
+    baseline["single_thread"] = oracle_rate(wl, 1, SINGLE_THREAD_SECONDS)[0]
     parity = None
     if timed_out is not None:
         got = np.asarray(timed_out[:n], dtype=np.float64)
@@ -576,9 +594,12 @@ def workload_line(wl, t, traffic):
     }
 
 
-def measure_workloads(A, torch, W, names, steps, warmup, workers, done, prewarm_ms):
+def measure_workloads(A, torch, W, names, steps, warmup, workers, done, prewarm_ms, oracle_1_thread=False,
+                      headline_oracle=None):
     """The other named workloads, each generated, timed like the headline one
-    and freed in turn (``done`` holds lines already measured)."""
+    and freed in turn (``done`` holds lines already measured).  With
+    oracle_1_thread every line also gets the fp64 oracle's one-thread rate on
+    a sample of its batch (``headline_oracle`` is the headline workload's)."""
     lines = dict(done)
     for name in names:
         if name in lines:
@@ -590,11 +611,17 @@ def measure_workloads(A, torch, W, names, steps, warmup, workers, done, prewarm_
         lines[name] = workload_line(wl, t, committed_traffic(name))
         if name == "c1":
             lines[name]["kind"] = "latency (13 MB: the batch fits in the caches)"
+        if oracle_1_thread:
+            lines[name]["cpu_baseline_1_thread"] = oracle_rate(wl, 1, SINGLE_THREAD_SECONDS)[0]
         log(f"workload {name}: {lines[name]['us_per_layer_step']} us/step, "
             f"kernel {lines[name]['kernel_us_mean']} us ({100 * lines[name]['kernel_frac']:.1f} %)")
         del wl
         torch.cuda.empty_cache()
-    return {k: lines[k] for k in names if k in lines}
+    out = {k: lines[k] for k in names if k in lines}
+    for k, v in out.items():
+        if oracle_1_thread and headline_oracle is not None and "cpu_baseline_1_thread" not in v:
+            v["cpu_baseline_1_thread"] = headline_oracle
+    return out
 
 
 def _timed(fn):
@@ -758,9 +785,11 @@ def main():
     if not args.no_workloads:
         del wl
         torch.cuda.empty_cache()
+        cb = result["cpu_baseline"]
         result["workloads"] = measure_workloads(A, torch, W, WORKLOADS, args.steps, args.warmup,
                                                 args.workers, {args.workload: headline_line},
-                                                args.prewarm_ms)
+                                                args.prewarm_ms, oracle_1_thread=cb is not None,
+                                                headline_oracle=cb["single_thread"] if cb else None)
     print(json.dumps(result), flush=True)
     if result["parity"] is not None and not result["parity"]["ok"]:
         print("bench.py: the timed output fails the parity bar against the oracle", file=sys.stderr)
