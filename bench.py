@@ -129,9 +129,9 @@ def committed_traffic(workload):
 
 def oracle_rate(wl, threads, target_s):
     """The fp64 oracle on `threads` host threads over the first requests of
-    the batch: one request first, then as many as take about target_s (at
-    most the whole batch).  Returns the rate line, the host case and the
-    oracle's output."""
+    the batch: one request first, then as many as its time per context
+    token puts at about target_s (at most the whole batch).  Returns the
+    rate line, the host case, the oracle's output and the request count."""
     import numpy as np
 
     import oracle
@@ -148,8 +148,9 @@ def oracle_rate(wl, threads, target_s):
     n = 1
     dt, case, ref = run(n)
     if dt < target_s and n < cfg.B:
-        per = dt / n
-        n = int(min(cfg.B, max(1, target_s / max(per, 1e-6))))
+        tokens = np.cumsum(np.maximum(np.asarray(wl.lens, dtype=np.int64), 0))
+        per_token = dt / max(1, int(tokens[0]))
+        n = int(max(1, min(cfg.B, np.searchsorted(tokens, target_s / per_token, side="right"))))
         dt, case, ref = run(n)
     nbytes = W.algorithmic_bytes(case.context_lens, n, cfg.Hq, cfg.Hkv, cfg.d)
     line = {
