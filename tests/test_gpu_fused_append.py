@@ -316,3 +316,44 @@ def test_fused_append_when_every_context_is_only_its_current_token_or_empty(torc
                 assert np.all(got[b] == 0)
         assert np.array_equal(kd.cpu().numpy().view(np.uint16), exp_k.view(np.uint16))
         assert np.array_equal(vd.cpu().numpy().view(np.uint16), exp_v.view(np.uint16))
+
+
+def test_fused_append_partition_32_and_64_bit_paths_agree(torch_cuda, apex, oracle_mod):
+    """The fused build on both sides of the kernel's 32-bit partition bound
+    (V (launched + 1) < 2^32, V = units on a forced grid).  255 requests of
+    4109 tokens: the partition covers the 4108 cached ones, 257 blocks each,
+    65535 units; 65536 work groups give 2^32 - 1 (32-bit), 65537 the 64-bit
+    path, with the same 65535 workers, so the outputs must agree bit for bit.
+    The first 256 blocks of every request repeat blocks of a shared pool; the
+    last one, which receives the current token, is the request's own."""
+    torch = torch_cuda
+    B, L, G, Hkv, pool = 255, 257 * 16 - 3, 1, 1, 1024
+    rng = np.random.default_rng(173)
+    q = rng.standard_normal((B, G * Hkv, D)).astype(np.float16)
+    kc = rng.standard_normal((pool + B, Hkv, BS, D)).astype(np.float16)
+    vc = rng.standard_normal((pool + B, Hkv, BS, D)).astype(np.float16)
+    table = np.empty((B, 257), dtype=np.int32)
+    table[:, :256] = rng.integers(0, pool, size=(B, 256))
+    table[:, 256] = pool + np.arange(B)
+    lens = np.full(B, L, dtype=np.int32)
+    kn = rng.standard_normal((B, Hkv, D)).astype(np.float16)
+    vn = rng.standard_normal((B, Hkv, D)).astype(np.float16)
+    slots = (pool + np.arange(B, dtype=np.int64)) * BS + (L - 1) % BS
+    kc[pool:, :, (L - 1) % BS:, :] = np.float16(np.nan)     # the current slots and past them
+    vc[pool:, :, (L - 1) % BS:, :] = np.float16(np.nan)
+    exp_k, exp_v = kv_cache.kv_append(kc, vc, kn, vn, slots)
+    assert (B * 257 * Hkv) * (65536 + 1) == 2**32 - 1
+    ref = oracle_mod.decode_attention_f64(q, exp_k, exp_v, table, lens, W.SCALE)
+    dev = "cuda"
+    outs = {}
+    for workers in (65536, 65537):
+        kd, vd = torch.from_numpy(kc).to(dev), torch.from_numpy(vc).to(dev)
+        out = apex.decode_attention_ex(torch.from_numpy(q).to(dev), kd, vd, torch.from_numpy(table).to(dev),
+                                       torch.from_numpy(lens).to(dev), W.SCALE, num_workers=workers,
+                                       k_new=torch.from_numpy(kn).to(dev), v_new=torch.from_numpy(vn).to(dev))
+        torch.cuda.synchronize()
+        outs[workers] = out.cpu().numpy()
+        check(outs[workers], ref, f"65535 units on {workers} work groups")
+        assert np.array_equal(kd.cpu().numpy().view(np.uint16), exp_k.view(np.uint16))
+        assert np.array_equal(vd.cpu().numpy().view(np.uint16), exp_v.view(np.uint16))
+    assert np.array_equal(outs[65536].view(np.uint16), outs[65537].view(np.uint16))

@@ -367,6 +367,11 @@ def test_partition_32_and_64_bit_paths_agree_at_the_bound(torch_cuda, apex, orac
     assert_parity(narrow, ref, "65535 units, 32-bit partition")
     assert_parity(wide, ref, "65535 units, 64-bit partition")
     assert np.array_equal(narrow.view(np.uint16), wide.view(np.uint16))
+    # the checked build shares the prologue: the same outputs on both paths
+    for workers in (65536, 65537):
+        got = run_gpu(torch_cuda, apex, case, num_workers=workers, check_inputs=True)
+        assert np.array_equal(got.view(np.uint16), narrow.view(np.uint16)), f"checked, {workers}"
+        assert apex.check_device_error() == 0
 
 
 # ---------------------------------------------------------------------------
