@@ -7,7 +7,8 @@
 // group
 //   1. reads context_lens once and derives the partition of plan_policy.h on
 //      its own (block sums, a prefix scan, the longest request for the tight
-//      block-table stride), so no planner kernel runs before it;
+//      block-table stride; 32-bit arithmetic unless the batch is too large
+//      for it), so no planner kernel runs before it;
 //   2. walks its contiguous range of (request b, kv-head g, block) units
 //      (ranges of equal cost, a pair's cost being its blocks plus a fixed
 //      start-up charge) segment by segment.  In a segment the four waves
