@@ -33,7 +33,10 @@
  *                block_table_stride (else one entry per request)
  *
  * Supported: d = 128, block_size = 16, Hq % Hkv == 0 with Hq / Hkv in
- * {1, 2, 4, 8}.  Anything else returns APEX_ERR_UNSUPPORTED.
+ * {1, 2, 4, 8}.  Anything else returns APEX_ERR_UNSUPPORTED.  The batch's
+ * block count, sum over b of ceil(L_b / block_size), must stay below 2^31
+ * (about 34 G context tokens): the kernel sums it in 32 bits.  The lengths
+ * are device data, so this is not checked.
  *
  * Precision: fp16 inputs, fp32 scores, softmax statistics and accumulation,
  * fp16 output rounded to nearest even.
