@@ -353,9 +353,42 @@ __device__ inline void new_token_logits(const AttnParams& p, const NewTokenRows<
     }
 }
 
+// The current token's K and V elements `dim` of kv-head g of request b and
+// the id of the block that holds its slot (position Lc - 1, Lc = the full
+// length), loaded ahead of the emit that needs them.  With the input check a
+// position past an explicit table row (a context cut to its row, already
+// reported) has no slot: the row's last slot holds a cached token.  The
+// slot's table entry is the same for the whole work group, so it is read
+// through the constant address space (the scalar path); `safe` is any
+// readable entry, read instead when there is no slot.
+// (The emit's loops give a thread elements idx = tid + k kAttnThreads, all
+// of one dim when kAttnThreads is a multiple of the head dimension.)
+static_assert(kAttnThreads % kHeadDim == 0, "a thread's emit elements share one dim");
+struct NewTokenElems {
+    f16 kn, vn;
+    int id;
+    bool in_row;
+};
+
+template <bool kCheck>
+__device__ inline NewTokenElems load_new_token_elems(const AttnParams& p, const int32_t* bt_row,
+                                                     const int32_t* safe, int b, int g, int Lc, int dim)
+{
+    NewTokenElems e;
+    const size_t src = (size_t)b * p.new_stride + (size_t)g * kHeadDim + dim;
+    e.kn = p.k_new[src];
+    e.vn = p.v_new[src];
+    e.in_row = !(kCheck && p.bt_stride > 0 && (int64_t)((Lc - 1) / kBlockSize) >= p.bt_stride);
+    const int32_t* a = e.in_row ? bt_row + (Lc - 1) / kBlockSize : safe;
+    e.id = *(const __attribute__((address_space(4))) int32_t*)a;
+    return e;
+}
+
 // Per-wave attention over its blocks of segment cs; ns is the work group's
 // next segment (n = 0 if none), `safe` any readable block-table entry, pf_next
-// whether the tiles continue into ns.  Lane
+// whether the tiles continue into ns, cur_row the block-table row of cs's
+// request (with the fused append, ne receives this thread's elements of the
+// current token for the emit: dim = thread index mod 128).  Lane
 // (h = lane % 16, q = lane / 16) keeps m (running max of head h, log2 units,
 // equal on the four lanes of h), l (sum of the weights of its tokens) and
 // acc[t][i] (running P.V of head h at dim 32q + 8i + t).  On return the
@@ -366,7 +399,7 @@ __device__ inline void wave_attend(const AttnParams& p, const WaveSeg& cs, const
                                    const int32_t* safe, bool pf_next, int L, WaveTiles& st, int wave,
                                    int lane,
                                    float (*s_acc)[G][kHeadDim], float (*s_m)[G], float (*s_l)[G],
-                                   float* s_new)
+                                   float* s_new, const int32_t* cur_row, NewTokenElems& ne)
 {
     constexpr int D = kHeadDim;
     constexpr int BS = kBlockSize;
@@ -405,14 +438,6 @@ __device__ inline void wave_attend(const AttnParams& p, const WaveSeg& cs, const
         st.nid0 = id_at(true, 2, n > 2);
         st.nid1 = id_at(true, 3, n > 3);
     }
-    // with the fused append, wave 0 computes the current token's logits for
-    // this pair here, the loads of its rows sharing the wait below (the merge
-    // reads them).  Every wave issues those loads, a few hundred bytes: with
-    // a branch on the wave around them, the compiler's wait placement cannot
-    // tell that every path passes the wait, and the loop's first waits would
-    // then cover the tiles too.
-    NewTokenRows<G> nt;
-    if (kAppend) load_new_token_rows<G>(p, cs.b, cs.g, lane, nt);
     // Everything loaded before the loop (the tiles, mostly issued during the
     // previous segment's last steps, and this segment's Q^T, issued one
     // segment ahead) is complete from here on, so the loop's own waits are
@@ -421,10 +446,21 @@ __device__ inline void wave_attend(const AttnParams& p, const WaveSeg& cs, const
 #ifdef APEX_TRACE_WORK_GROUPS
     if (wave == 0 && lane == 0 && s_trace[2] == 0) s_trace[2] = trace_clock();
 #endif
-    if (kAppend && uniform(wave) == 0) new_token_logits<G>(p, nt, lane, s_new);
 #pragma unroll
     for (int i = 0; i < 4; ++i) st.qop[i] = st.qnext[i];
     load_q<G>(st.qnext, ns, lane);   // used by the next segment only
+    // With the fused append: the rows of the current token's logits for this
+    // pair (wave 0 sums them after the loop; the merge reads them) and this
+    // thread's elements for the emit.  Issued after the wait above, they
+    // complete during the block loop instead of adding a round trip to the
+    // segment's entry and to its emit.  Every wave issues the row loads, a
+    // few hundred bytes: with a branch on the wave around them the compiler's
+    // wait placement could not tell that every path passes the loop's waits.
+    NewTokenRows<G> nt;
+    if (kAppend) {
+        load_new_token_rows<G>(p, cs.b, cs.g, lane, nt);
+        ne = load_new_token_elems<kCheck>(p, cur_row, safe, cs.b, cs.g, L + 1, (wave * 64 + lane) % D);
+    }
 
     float m = -INFINITY, l = 0.f;
     f32x4 acc[8];
@@ -549,6 +585,7 @@ __device__ inline void wave_attend(const AttnParams& p, const WaveSeg& cs, const
     }
     if (k < n) block_step(st.kt0, st.vt0, k, st.cur0, st.nid0);
     st.prefetched = pf;
+    if (kAppend && uniform(wave) == 0) new_token_logits<G>(p, nt, lane, s_new);
 
     // the wave's state for head h: l summed over the four token groups
     const float lw = rows_sum4(l);
@@ -589,25 +626,19 @@ __device__ inline void fold_new_token(float sn, float vn, float& M, float& num, 
     M = M2;
 }
 
-// Writes element `dim` of the current token's K and V rows of kv-head g to
-// its cache slot: position Lc - 1 of request b (Lc = the full length).  With
-// the input check, a position past an explicit table row (a context cut to
-// its row, already reported) is not stored: the row's last slot holds a
-// cached token.
+// Writes those elements to the slot (with the input check, a block id outside
+// the pool is reported and not written).
 template <bool kCheck>
-__device__ inline void store_new_token(const AttnParams& p, const int32_t* bt_row, int b, int g, int Lc,
-                                       int dim)
+__device__ inline void store_new_token(const AttnParams& p, const NewTokenElems& e, int g, int Lc, int dim)
 {
-    if (kCheck && p.bt_stride > 0 && (int64_t)((Lc - 1) / kBlockSize) >= p.bt_stride) return;
-    const int id = bt_row[(Lc - 1) / kBlockSize];
-    if (kCheck && !(id >= 0 && (int64_t)id < p.num_blocks)) {
+    if (!e.in_row) return;
+    if (kCheck && !(e.id >= 0 && (int64_t)e.id < p.num_blocks)) {
         if (dim == 0) report_error(p, kErrBlockId);
         return;
     }
-    const size_t dst = (((size_t)(uint32_t)id * p.Hkv + g) * kBlockSize + (Lc - 1) % kBlockSize) * kHeadDim + dim;
-    const size_t src = (size_t)b * p.new_stride + (size_t)g * kHeadDim + dim;
-    p.k_store[dst] = p.k_new[src];
-    p.v_store[dst] = p.v_new[src];
+    const size_t dst = (((size_t)(uint32_t)e.id * p.Hkv + g) * kBlockSize + (Lc - 1) % kBlockSize) * kHeadDim + dim;
+    p.k_store[dst] = e.kn;
+    p.v_store[dst] = e.vn;
 }
 
 template <int G, bool kCheck, bool kAppend>
@@ -834,9 +865,11 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
         if (more)
             ns = wave_seg<G>(p, bt + (size_t)uniform(b2) * (size_t)stride, b2, g2, blk2, blk2 + take2, wave,
                              lane);
+        NewTokenElems ne;
         wave_attend<G, kCheck, kAppend>(p, cs, ns, bt,
                                         more && take >= kPrefetchBlocks && take2 >= kPrefetchBlocks, L,
-                                        st, wave, lane, s_acc, s_m, s_l, s_new);
+                                        st, wave, lane, s_acc, s_m, s_l, s_new,
+                                        bt + (size_t)uniform(b) * (size_t)stride, ne);
         __syncthreads();
 #ifdef APEX_TRACE_WORK_GROUPS
         if (tid == 0) {
@@ -864,9 +897,8 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
             }
             if (wf == wl) {
                 if (append) {
-                    const size_t nrow = (size_t)b * p.new_stride + (size_t)g * D;
-                    fold_new_token(s_new[h], (float)p.v_new[nrow + dim], M, num, den);
-                    if (h == 0) store_new_token<kCheck>(p, bt + (size_t)b * stride, b, g, L + 1, dim);
+                    fold_new_token(s_new[h], (float)ne.vn, M, num, den);
+                    if (h == 0) store_new_token<kCheck>(p, ne, g, L + 1, dim);
                 }
                 write_row(p, b, g * G + h, dim, M, num, den);
             } else {
@@ -936,9 +968,8 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
                         M = Mn;
                     }
                     if (append) {
-                        const size_t nrow = (size_t)b * p.new_stride + (size_t)g * D;
-                        fold_new_token(s_new[h], (float)p.v_new[nrow + dim], M, num, den);
-                        if (h == 0) store_new_token<kCheck>(p, bt + (size_t)b * stride, b, g, L + 1, dim);
+                        fold_new_token(s_new[h], (float)ne.vn, M, num, den);
+                        if (h == 0) store_new_token<kCheck>(p, ne, g, L + 1, dim);
                     }
                     write_row(p, b, g * G + h, dim, M, num, den);
                 }
@@ -981,7 +1012,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
                 }
             }
             for (int i = tid; i < p.Hkv * D; i += kAttnThreads)
-                store_new_token<kCheck>(p, bt + (size_t)b * stride, b, i / D, 1, i % D);
+                store_new_token<kCheck>(
+                    p, load_new_token_elems<kCheck>(p, bt + (size_t)b * stride, bt, b, i / D, 1, i % D), i / D, 1,
+                    i % D);
         } else {
             for (int i = tid; i < p.Hq * D; i += kAttnThreads) write_row(p, b, i / D, i % D, 0.f, 0.f, 0.f);
         }
