@@ -195,11 +195,13 @@ def test_fused_append_full_size_whole_tensor(torch_cuda, apex, oracle_mod, name)
     torch.cuda.empty_cache()
 
 
-def test_fused_append_checked_path_bad_current_block(torch_cuda, apex, oracle_mod):
+@pytest.mark.parametrize("workers", [0, 1, 3, 40])
+def test_fused_append_checked_path_bad_current_block(torch_cuda, apex, oracle_mod, workers):
     """The checked path when the current token's own table entry is outside
     the pool: the error bit is set and nothing is stored; that block's cached
     tokens are skipped like any bad block, and the current token is still
-    attended from the new rows."""
+    attended from the new rows.  Forced grids split the pairs, so the emit is
+    also the last arriver's (40 work groups: about one unit each)."""
     torch = torch_cuda
     lens = [40, 17]
     G, Hkv = 4, 8
@@ -231,11 +233,11 @@ def test_fused_append_checked_path_bad_current_block(torch_cuda, apex, oracle_mo
     kd, vd = torch.from_numpy(kc).to(dev), torch.from_numpy(vc).to(dev)
     out = apex.decode_attention_ex(torch.from_numpy(case.q).to(dev), kd, vd, torch.from_numpy(bt).to(dev),
                                    torch.from_numpy(case.context_lens).to(dev), case.scale,
-                                   check_inputs=True, k_new=torch.from_numpy(kn).to(dev),
+                                   check_inputs=True, num_workers=workers, k_new=torch.from_numpy(kn).to(dev),
                                    v_new=torch.from_numpy(vn).to(dev))
     torch.cuda.synchronize()
     assert apex.check_device_error() == apex.DEVICE_ERR_BLOCK_ID
-    check(out.cpu().numpy(), ref, "bad current block")
+    check(out.cpu().numpy(), ref, f"bad current block, workers={workers}")
     assert np.array_equal(kd.cpu().numpy().view(np.uint16), exp_k.view(np.uint16))
     assert np.array_equal(vd.cpu().numpy().view(np.uint16), exp_v.view(np.uint16))
 
