@@ -513,7 +513,7 @@ __device__ inline void wave_attend(const AttnParams& p, const WaveSeg& cs, const
         float sv[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) sv[i] = s[i] * p.scale_log2;
-        const bool tail = tok0 + BS > L;   // the pair's last, partial block
+        const bool tail = tok0 > L - BS;   // the pair's last, partial block (no overflow at L near 2^31)
         if (tail) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)

@@ -375,6 +375,62 @@ def test_partition_32_and_64_bit_paths_agree_at_the_bound(torch_cuda, apex, orac
 
 
 # ---------------------------------------------------------------------------
+# the longest context an int32 length allows, 2^31 - 1 tokens (2^27 blocks):
+# the table repeats block 0 and ends on block 1, whose slot 15 (past the
+# context) holds NaN.  Expected values from the multiset form
+# (tests/multiset_attention.py, checked against the oracle on the CPU).
+# ---------------------------------------------------------------------------
+
+def test_longest_context_int32(torch_cuda, apex):
+    import multiset_attention as MS
+    torch = torch_cuda
+    L = 2**31 - 1
+    nb = -(-L // W.BLOCK_SIZE)
+    assert nb == 2**27 and L - W.BLOCK_SIZE * (nb - 1) == 15
+    G, Hkv = 4, 1
+    rng = np.random.default_rng(2**31 % 1000)
+    q = rng.standard_normal((1, G * Hkv, W.D_HEAD)).astype(np.float16)
+    k = rng.standard_normal((2, Hkv, W.BLOCK_SIZE, W.D_HEAD)).astype(np.float16)
+    v = rng.standard_normal((2, Hkv, W.BLOCK_SIZE, W.D_HEAD)).astype(np.float16)
+    k[1, :, 15, :] = np.float16(np.nan)
+    v[1, :, 15, :] = np.float16(np.nan)
+    table = np.zeros((1, nb), dtype=np.int32)
+    table[0, -1] = 1
+    ref = MS.multiset_attention(q[0], k, v, table[0], L, W.SCALE)[None]
+    dev = "cuda"
+    qd, kd, vd = (torch.from_numpy(x).to(dev) for x in (q, k, v))
+    bt = torch.from_numpy(table).to(dev)
+    cl = torch.tensor([L], dtype=torch.int32, device=dev)
+    # Every wave sums its blocks in fp32; with one block repeated, the rounding
+    # of those sums does not average out and grows with the blocks per wave:
+    # 2^16 on the default grid (512 work groups here), 2^15 on 1024.  (A
+    # forced grid of 256 takes 2^17 per wave and leaves the bar: rel-L2
+    # about 1.5e-3.)
+    for workers in (0, 1024):
+        out = apex.decode_attention_ex(qd, kd, vd, bt, cl, W.SCALE, num_workers=workers)
+        torch.cuda.synchronize()
+        assert_parity(out.cpu().numpy(), ref, f"L = 2^31 - 1, workers={workers}")
+    # the fused append: 2^31 - 2 cached tokens and the current one, stored at
+    # slot 14 of block 1
+    kn = rng.standard_normal((1, Hkv, W.D_HEAD)).astype(np.float16)
+    vn = rng.standard_normal((1, Hkv, W.D_HEAD)).astype(np.float16)
+    k_exp, v_exp = k.copy(), v.copy()
+    k_exp[1, :, 14, :] = kn[0]
+    v_exp[1, :, 14, :] = vn[0]
+    ref = MS.multiset_attention(q[0], k_exp, v_exp, table[0], L, W.SCALE)[None]
+    k_in, v_in = k.copy(), v.copy()
+    k_in[1, :, 14, :] = np.float16(np.nan)
+    v_in[1, :, 14, :] = np.float16(np.nan)
+    kd, vd = torch.from_numpy(k_in).to(dev), torch.from_numpy(v_in).to(dev)
+    out = apex.decode_attention_ex(qd, kd, vd, bt, cl, W.SCALE, k_new=torch.from_numpy(kn).to(dev),
+                                   v_new=torch.from_numpy(vn).to(dev))
+    torch.cuda.synchronize()
+    assert_parity(out.cpu().numpy(), ref, "L = 2^31 - 1, fused append")
+    assert np.array_equal(kd.cpu().numpy().view(np.uint16), k_exp.view(np.uint16))
+    assert np.array_equal(vd.cpu().numpy().view(np.uint16), v_exp.view(np.uint16))
+
+
+# ---------------------------------------------------------------------------
 # input check (APEX_DECODE_FLAG_CHECK_INPUTS)
 # ---------------------------------------------------------------------------
 

@@ -336,3 +336,49 @@ def test_planted_mistakes(oracle_mod):
                 pkg._LIB = saved
                 pkg._build.LIB = saved_path
             assert caught, f"planted mistake '{name}' passed every pin"
+
+
+# ---------------------------------------------------------------------------
+# the multiset form of attention over a table that repeats blocks
+# (tests/multiset_attention.py), which stands in for the oracle on contexts
+# too long for its loop
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("G,Hkv", [(1, 1), (4, 1), (2, 3)])
+def test_multiset_form_matches_the_oracle_on_repeating_tables(oracle_mod, G, Hkv):
+    import multiset_attention as MS
+    rng = np.random.default_rng(300 + 10 * G + Hkv)
+    pool, bs, d = 5, 16, 128
+    k = rng.standard_normal((pool, Hkv, bs, d)).astype(np.float16)
+    v = rng.standard_normal((pool, Hkv, bs, d)).astype(np.float16)
+    for trial in range(6):
+        L = int(rng.integers(1, 40 * bs))
+        nb = -(-L // bs)
+        table = rng.integers(0, pool, size=(1, nb + 2)).astype(np.int32)
+        if trial % 2:
+            table[0, :nb - 1] = 0                 # one block repeated, another at the end
+            table[0, nb - 1] = 1
+        q = rng.standard_normal((1, G * Hkv, d)).astype(np.float16)
+        scale = float(np.float32(1.0 / math.sqrt(d)))
+        ref = oracle_mod.decode_attention_f64(q, k, v, table, np.array([L], dtype=np.int32), scale)[0]
+        got = MS.multiset_attention(q[0], k, v, table[0], L, scale)
+        assert np.allclose(got, ref, rtol=0, atol=1e-12), (trial, L)
+
+
+def test_multiset_form_counts_and_a_planted_miscount(oracle_mod):
+    """Token counts of a ragged table written out by hand; one count off is
+    visible in the attention."""
+    import multiset_attention as MS
+    c = MS.token_counts(np.array([2, 0, 2, 1], dtype=np.int32), 3 * 16 + 5, 16, 3)
+    assert c[2].tolist() == [2.0] * 16
+    assert c[0].tolist() == [1.0] * 16
+    assert c[1].tolist() == [1.0] * 5 + [0.0] * 11
+    rng = np.random.default_rng(7)
+    k = rng.standard_normal((3, 1, 16, 128)).astype(np.float16)
+    v = rng.standard_normal((3, 1, 16, 128)).astype(np.float16)
+    q = rng.standard_normal((1, 1, 128)).astype(np.float16)
+    table = np.array([[2, 0, 2, 1]], dtype=np.int32)
+    ref = oracle_mod.decode_attention_f64(q, k, v, table, np.array([53], dtype=np.int32), 0.125)[0]
+    assert np.allclose(MS.multiset_attention(q[0], k, v, table[0], 53, 0.125), ref, rtol=0, atol=1e-12)
+    # a context one token longer counts slot 5 of block 1 once more
+    assert not np.allclose(MS.multiset_attention(q[0], k, v, table[0], 54, 0.125), ref, rtol=0, atol=1e-6)
