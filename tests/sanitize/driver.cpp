@@ -8,7 +8,9 @@
 //     whole and chunked pairs, several thread counts and pool resizes;
 //   - the partition's host mirror, against an explicit line of positions
 //     (every non-empty pair's cost positions, then its blocks);
-//   - the strategy selection (Eq. 1-8, Alg. 1-2) on random valid inputs.
+//   - the strategy selection (Eq. 1-8, Alg. 1-2) on random valid inputs;
+//   - the partition's 32-bit arithmetic (the kernel's path when
+//     V (launched + 1) < 2^32) against its 64-bit form.
 // Usage: driver <cases> <mode: all | threads>; exit status 0 when every
 // check holds.
 #include <immintrin.h>
@@ -25,6 +27,7 @@
 #include "apex_cpu_attention.h"
 #include "apex_decode.h"
 #include "apex_sched.h"
+#include "plan_policy.h"
 
 extern "C" int apex_oracle_decode_attention_f64(const uint16_t* q, const uint16_t* k_cache,
                                                 const uint16_t* v_cache, const int32_t* block_table,
@@ -175,6 +178,42 @@ void partition_case(std::mt19937_64& rng)
     check(partials == split, "partials", (long)partials, (long)split);
 }
 
+// One case of the partition in 32-bit arithmetic, drawn inside the bound the
+// kernel uses it under (V (launched + 1) <= 2^32 - 1, half the draws close to
+// it): the worker count and every sampled range end must equal the 64-bit
+// form's.
+void width_case(std::mt19937_64& rng)
+{
+    std::uniform_int_distribution<int64_t> pick(0, (int64_t)1 << 40);
+    const int64_t launched = 1 + pick(rng) % ((int64_t)1 << 20);
+    const int64_t max_v = (int64_t)(0xffffffffull / (uint64_t)(launched + 1));
+    const int64_t K = pick(rng) % 2 ? 8 : 0;
+    int64_t units = 0, pairs = 0;
+    for (int tries = 0; tries < 100; ++tries) {
+        units = pick(rng) % 2 ? max_v - pick(rng) % 64 : 1 + pick(rng) % std::max<int64_t>(1, max_v);
+        if (units < 1) continue;
+        pairs = 1 + pick(rng) % units;
+        if (units + K * pairs <= max_v) break;
+        units = 0;
+    }
+    if (units == 0) return;
+    const int64_t V = units + K * pairs;
+    check((uint64_t)V * (uint64_t)(launched + 1) <= 0xffffffffull, "width case outside the bound", (long)V);
+    const int64_t cus = pick(rng) % 2 ? 256 : 0;
+    const int min_units = pick(rng) % 2 ? 16 : 1;
+    const int64_t W = apex::active_workers(units, launched, min_units, pairs, cus);
+    const uint32_t W32 = apex::active_workers_t<uint32_t>((uint32_t)units, (uint32_t)launched, (uint32_t)min_units,
+                                                          (uint32_t)pairs, (uint32_t)cus);
+    check((int64_t)W32 == W, "32-bit worker count", (long)W32, (long)W);
+    for (int i = 0; i < 16; ++i) {
+        const int64_t w = i < 2 ? (i == 0 ? 0 : W - 1) : pick(rng) % W;
+        for (int64_t e = w; e <= w + 1; ++e) {
+            const uint32_t end32 = (uint32_t)e * (uint32_t)V / W32;   // the kernel's 32-bit range end
+            check((int64_t)end32 == apex::worker_start(e, V, W), "32-bit range end", (long)e, (long)end32);
+        }
+    }
+}
+
 // One strategy-selection case on random valid inputs (exercised for
 // undefined behaviour; the decisions are checked against the oracle in
 // tests/test_sched.py).
@@ -218,6 +257,7 @@ int main(int argc, char** argv)
         if (!threads_only) {
             partition_case(rng);
             sched_case(rng);
+            for (int j = 0; j < 20; ++j) width_case(rng);
         }
     }
     printf("%d cases, %d failures\n", cases, g_failures);
