@@ -64,6 +64,11 @@ CONFIGS = {
                  4, 32, 32, 8, lens="lognormal", lo=4096, hi=32768),
     "c5": Config("c5", "Llama-3.1-8B GQA memory-pressure mixed batch, B=512, L half U[256,1024] half U[4096,16384], paged bs=16",
                  5, 512, 32, 8, lens="bimodal", placement="random", key_offset_std=0.5),
+    # parity shapes beyond the five workloads: the other two group sizes at full size
+    "g8": Config("g8", "GQA G=8 (Llama-3-70B heads, 64 q over 8 kv), B=32, c4's lengths, paged bs=16",
+                 6, 32, 64, 8, lens="lognormal", lo=4096, hi=32768),
+    "g2": Config("g2", "GQA G=2 (32 q over 16 kv), B=128, c3's lengths, paged bs=16",
+                 7, 128, 32, 16, lens="uniform", lo=1024, hi=4096),
 }
 
 

@@ -280,6 +280,23 @@ def test_full_size_whole_tensor_parity(torch_cuda, apex, oracle_mod, name):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("name", ["g8", "g2"])
+def test_full_size_whole_tensor_parity_other_group_sizes(torch_cuda, apex, oracle_mod, name):
+    """The two group sizes the five workloads do not use, at full size and in
+    the benchmark's launch configuration: G = 8 (Llama-3-70B heads) with the
+    long-output lengths, G = 2 with the GQA decode lengths; whole tensor."""
+    torch = torch_cuda
+    print(f"[full-size] generating {name}", flush=True)
+    wl = W.DeviceWorkload(name)
+    ref = whole_tensor.oracle_reference(oracle_mod, wl)
+    apex.decode_attention(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens,
+                          wl.scale, out=wl.out)
+    torch.cuda.synchronize()
+    whole_tensor.assert_whole_tensor(wl.out.cpu().numpy(), ref, name)
+    del wl
+    torch.cuda.empty_cache()
+
+
 # ---------------------------------------------------------------------------
 # batches past the lengths the kernel keeps in LDS (2048 requests), and one
 # request split over ~100 work groups (combine in several chunks of 8)
