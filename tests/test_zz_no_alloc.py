@@ -168,3 +168,19 @@ def test_noalloc_captured_in_a_graph_and_replayed(torch_cuda, apex):
     graph.replay()
     torch.cuda.synchronize()
     assert torch.equal(out.view(torch.int16), ref2.view(torch.int16)), "replay after a new query"
+
+
+@pytest.mark.parametrize("name", ["c4", "c5"])
+def test_noalloc_full_size_workload_equals_the_base_call(torch_cuda, apex, name):
+    """A full workload in the benchmark's shape (c4: 32 x 8 pairs, c5: 512 x 8)
+    through the static array: the default grid fits it (512 work groups of
+    G = 4 under its 1024), so the result is the base call's bit for bit."""
+    torch = torch_cuda
+    wl = W.DeviceWorkload(name)
+    base = apex.decode_attention(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens, wl.scale)
+    out = torch.full_like(base, float("nan"))
+    apex.decode_attention_noalloc(wl.q, wl.k_cache, wl.v_cache, wl.block_table, wl.context_lens, wl.scale, out)
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), base.view(torch.int16))
+    del wl, base, out
+    torch.cuda.empty_cache()
